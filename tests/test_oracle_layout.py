@@ -1,0 +1,148 @@
+"""Pins of the oracle's placement and validation rules (oracle/layout.py)."""
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+from oracle.layout import (EHOLE, EINVAL, ENOMEM, EOVERLAP, ERANGE, ESTATE, FcgError, Layout)
+
+
+def _lay(**kw):
+    args = dict(n_layers=2, n_seqs=2, max_tokens=16, page_size=0, n_pages=0,
+                seg_len=[3, 5, 2], seg_src_pos0=[0, 0, 4])
+    args.update(kw)
+    return Layout(**args)
+
+
+def test_contiguous_placement_by_hand():
+    L = _lay()
+    res = L.graft([0, 0], [1, 0], [0, 5])
+    # seg 1 (5 tokens, source at 0) at 0 -> delta 0; seg 0 (3 tokens) at 5 -> delta 5
+    assert res == [(0, 1, 0, 0), (0, 0, 5, 5)]
+    assert L.written[0].tolist() == [[True] * 8 + [False] * 8] * 2
+    assert not L.written[1].any()
+    assert L.seq_len(0, 0) == 8 and L.seq_len(0, 1) == 8
+    # seg 2 was captured at source position 4: grafted at 10 it turns by 6
+    assert L.graft([1], [2], [10]) == [(1, 2, 10, 6)]
+    # fresh tokens at 8, 9 of layer 1 only; decode then appends at the length
+    L.append(1, [0, 0], [9, 8])
+    assert L.seq_len(0, 1) == 10 and L.seq_len(0, 0) == 8
+    assert L.decode(1, [0]) == [10]
+    assert L.decode(0, [0]) == [8]
+    assert L.slot(0, 7) == (-1, 7)
+
+
+def test_paged_assignment_by_hand():
+    L = _lay(page_size=4, n_pages=6, max_tokens=16)
+    # one call: seq 1 gets seg 1 at 2 (positions 2..6, logical pages 0, 1); seq 0 gets seg 0 at 0 (page 0)
+    L.graft([1, 0], [1, 0], [2, 0])
+    # mapped in ascending (seq, logical page): (0,0)->0, (1,0)->1, (1,1)->2
+    assert L.page_table.tolist() == [[0, -1, -1, -1], [1, 2, -1, -1]]
+    # seq 0, layer 0: positions 3 (page 0, mapped) and 4 (logical page 1, new) -> physical 3
+    L.append(0, [0, 0], [3, 4])
+    assert L.page_table[0].tolist() == [0, 3, -1, -1]
+    assert L.slot(0, 4) == (3, 0) and L.slot(1, 6) == (2, 2)
+    # decode on seq 0 layer 0 appends at 5 (logical page 1, mapped: nothing new)
+    assert L.decode(0, [0]) == [5]
+    # seq 1 has positions 0, 1 unwritten: decoding it would read a hole
+    with pytest.raises(FcgError) as e:
+        L.decode(0, [1])
+    assert e.value.code == EHOLE
+    # releasing seq 1 frees 1 and 2; the next new page takes the lowest free one
+    L.reset(1)
+    assert L.page_table[1].tolist() == [-1] * 4
+    L.graft([1], [2], [8])                      # positions 8, 9 -> logical page 2
+    assert L.page_table[1].tolist() == [-1, -1, 1, -1]
+    L.graft([0], [2], [12])                     # logical page 3 of seq 0 -> physical 2
+    assert L.page_table[0].tolist() == [0, 3, -1, 2]
+
+
+@pytest.mark.parametrize("call,code", [
+    (lambda L: L.graft([0], [0], [0, 1]), EINVAL),
+    (lambda L: L.decode(0, [0, 0]), EINVAL),
+    (lambda L: L.graft([2], [0], [0]), ERANGE),
+    (lambda L: L.graft([0], [3], [0]), ERANGE),
+    (lambda L: L.graft([0], [1], [-1]), ERANGE),
+    (lambda L: L.graft([0], [1], [12]), ERANGE),          # 12 + 5 > 16
+    (lambda L: L.append(2, [0], [0]), ERANGE),
+    (lambda L: L.append(0, [0], [16]), ERANGE),
+    (lambda L: L.decode(0, [1]), ESTATE),
+    (lambda L: L.graft([0, 0], [0, 1], [0, 2]), EOVERLAP),
+    (lambda L: L.append(0, [0, 0], [0, 0]), EOVERLAP),
+    (lambda L: L.append(0, [0], [1]), EHOLE),             # position 0 unwritten
+])
+def test_error_classes_on_empty_cache(call, code):
+    L = _lay()
+    before = (L.written.copy(), L.page_table.copy())
+    with pytest.raises(FcgError) as e:
+        call(L)
+    assert e.value.code == code
+    np.testing.assert_array_equal(L.written, before[0])
+    np.testing.assert_array_equal(L.page_table, before[1])
+
+
+def test_error_classes_after_graft():
+    L = _lay()
+    L.graft([0], [1], [0])                                # 0..4 in both layers
+    with pytest.raises(FcgError) as e:
+        L.graft([0], [0], [4])                            # meets written position 4
+    assert e.value.code == EOVERLAP
+    with pytest.raises(FcgError) as e:
+        L.append(1, [0], [3])
+    assert e.value.code == EOVERLAP
+    with pytest.raises(FcgError) as e:
+        L.append(0, [0], [6])                             # 5 unwritten
+    assert e.value.code == EHOLE
+    L.graft([0], [2], [7])                                # 7, 8 written; 5, 6 are a hole
+    with pytest.raises(FcgError) as e:
+        L.decode(0, [0])
+    assert e.value.code == EHOLE
+    L.append(0, [0, 0], [5, 6])
+    assert L.decode(0, [0]) == [9]
+
+
+def test_page_pool_exhaustion_changes_nothing():
+    L = _lay(page_size=4, n_pages=2)
+    L.graft([0], [1], [0])                                # pages 0, 1 (positions 0..4)
+    before = L.page_table.copy()
+    with pytest.raises(FcgError) as e:
+        L.graft([1], [0], [0])
+    assert e.value.code == ENOMEM
+    np.testing.assert_array_equal(L.page_table, before)
+    assert not L.written[1].any()
+    L.reset(0)
+    L.graft([1], [0], [0])
+    assert L.page_table[1, 0] == 0
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_random_plans_against_enumeration(data):
+    n_seg = data.draw(st.integers(1, 6))
+    seg_len = data.draw(st.lists(st.integers(1, 9), min_size=n_seg, max_size=n_seg))
+    src = data.draw(st.lists(st.integers(0, 50), min_size=n_seg, max_size=n_seg))
+    page = data.draw(st.sampled_from([0, 4, 16]))
+    L = Layout(3, 2, 64, page, 64, seg_len, src)
+    occupied = {0: set(), 1: set()}
+    pages_used = 0
+    for _ in range(data.draw(st.integers(1, 5))):
+        seq = data.draw(st.integers(0, 1))
+        seg = data.draw(st.integers(0, n_seg - 1))
+        dst = data.draw(st.integers(0, 64 - seg_len[seg]))
+        span = set(range(dst, dst + seg_len[seg]))
+        ok = not (span & occupied[seq])
+        try:
+            res = L.graft([seq], [seg], [dst])
+            assert ok
+            assert res == [(seq, seg, dst, dst - src[seg])]
+            occupied[seq] |= span
+        except FcgError as e:
+            assert not ok and e.code == EOVERLAP
+    for seq in (0, 1):
+        for layer in range(3):
+            assert set(np.flatnonzero(L.written[seq, layer]).tolist()) == occupied[seq]
+    if page:
+        mapped = L.page_table[L.page_table >= 0]
+        assert len(set(mapped.tolist())) == len(mapped)            # injective
+        # exactly the touched logical pages are mapped, and they use pages 0..k-1
+        want = sum(len({p // page for p in occupied[s]}) for s in (0, 1))
+        assert len(mapped) == want and sorted(mapped.tolist()) == list(range(want))
