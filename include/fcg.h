@@ -1,0 +1,185 @@
+/*
+ * fcg.h - function-level KV cache grafting on one MI355X (gfx950).
+ *
+ * C ABI of libfcg.so.  The library holds a segment library of function-level
+ * KV states (the two-tier code cache of Sec. 4.1, Eq. 2: every function entry
+ * keeps the KV states of its interface and of its implementation), stitches
+ * retrieved segments into a composite cache at new positions (cache-stitching,
+ * Sec. 4.2, Eq. 4: the interface KV states are concatenated and injected as
+ * context), prefills patch tokens over that cache and decodes (cache-patching,
+ * Sec. 4.2, Eq. 6: the prefix KV states are reused and only the new span is
+ * computed).  Text, tokenizer and model weights are outside this library; its
+ * inputs are token-level K/V/Q tensors.
+ *
+ * Conventions
+ *  - Every entry point returns an fcg_status; nothing aborts or throws across
+ *    the ABI.  fcg_last_error() gives a thread-local message for the last
+ *    failing call on the calling thread.
+ *  - A call that returns an error changes no state.
+ *  - "device" pointers are HIP device memory on the current device; "host"
+ *    pointers are ordinary host memory, read (or written) before the call
+ *    returns.  The caller keeps ownership of everything it passes.
+ *  - stream is a hipStream_t (NULL = the default stream).  Calls validate on
+ *    the host, enqueue their kernels on the stream and return; results are
+ *    ready when the stream reaches that point.  A handle (fcg_lib, fcg_cache)
+ *    must not be used by two threads or two streams at the same time.
+ *  - Device faults of earlier work surface as FCG_EHIP from a later call.
+ *  - Storage dtype: FCG_F32 = IEEE binary32, FCG_BF16 = bfloat16 (raw 16-bit
+ *    patterns).  Every narrowing rounds to nearest, ties to even.
+ *
+ * Tensor layouts (elements of the storage dtype, row-major, innermost last)
+ *  - Segment input to fcg_lib_add_segment:   k, v  [L][len][Hkv][D]
+ *  - Library slab of one layer:              [Hkv][capacity][D]
+ *  - Contiguous cache, one layer:            [n_seqs][Hkv][max_tokens][D]
+ *  - Paged cache, one layer:                 [n_pages][Hkv][page_size][D]
+ *  - Fresh tokens of fcg_patch_prefill:      q [n][Hq][D], k, v [n][Hkv][D]
+ *  - Decode tokens of fcg_decode:            q [n][Hq][D], k, v [n][Hkv][D]
+ *  - Attention outputs:                      out [n][Hq][D]
+ */
+#ifndef FCG_H
+#define FCG_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FCG_OK = 0,
+  FCG_EINVAL = 1,   /* malformed argument: null pointer, bad count, unsupported shape, mismatch */
+  FCG_ERANGE = 2,   /* index out of range: layer, sequence, segment, position, span end */
+  FCG_EOVERLAP = 3, /* a target position is given twice or is already written */
+  FCG_EHOLE = 4,    /* attention would read a position that is not written */
+  FCG_ENOMEM = 5,   /* device memory, library capacity or page pool exhausted */
+  FCG_ESTATE = 6,   /* operation not valid in the current state (e.g. decode on an empty sequence) */
+  FCG_EHIP = 7      /* the HIP runtime reported an error */
+} fcg_status;
+
+typedef enum { FCG_F32 = 0, FCG_BF16 = 1 } fcg_dtype;
+
+/* Shape of the attention layers whose KV states are grafted.  Keys carry the
+ * rotary position encoding in rotate-half layout: dimension i and i + D/2 turn
+ * together by p * theta^(-2i/D) at position p (rope_style 0, the only one). */
+typedef struct {
+  int32_t n_layers;   /* L >= 1 */
+  int32_t n_q_heads;  /* Hq, a multiple of Hkv; Hq / Hkv <= 16 */
+  int32_t n_kv_heads; /* Hkv >= 1 */
+  int32_t head_dim;   /* D: 64 or 128 */
+  double rope_theta;  /* theta > 1 */
+  int32_t dtype;      /* fcg_dtype of every K, V, Q and output tensor */
+  int32_t rope_style; /* 0 = rotate-half */
+} fcg_model_desc;
+
+typedef struct fcg_lib fcg_lib;
+typedef struct fcg_cache fcg_cache;
+
+/* ---------------------------------------------------------------- library */
+
+/* flags of fcg_lib_create and fcg_cache_create */
+#define FCG_LAYOUT_ONLY 1u /* no device memory: only the index / layout is kept (planning and tests) */
+
+/* Create an empty segment library (the KV side of the two-tier code cache,
+ * Sec. 4.1, Eq. 2) holding up to capacity_tokens tokens in up to max_segments
+ * segments.  Allocates L * Hkv * capacity_tokens * D elements for K and as
+ * many for V (none with FCG_LAYOUT_ONLY: then only the segment index exists,
+ * segments are added with k == v == NULL, and grafts into layout-only caches
+ * are planned but move nothing).  FCG_ENOMEM if the device cannot hold them. */
+fcg_status fcg_lib_create(const fcg_model_desc* desc, int64_t capacity_tokens,
+                          int32_t max_segments, uint32_t flags, fcg_lib** out);
+
+/* Append one segment of len tokens whose keys were encoded at source positions
+ * src_pos0 .. src_pos0 + len - 1.  k, v: device [L][len][Hkv][D], copied into
+ * the slabs on stream.  k == v == NULL reserves the space only (the caller
+ * fills it through fcg_lib_device_ptrs).  *seg_id receives the new id
+ * (ids are 0, 1, 2, ... in order of addition).  FCG_ENOMEM when capacity or
+ * max_segments is exhausted. */
+fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, const void* k,
+                               const void* v, void* stream, int32_t* seg_id);
+
+/* Where segment seg_id sits: tokens tok_off .. tok_off + len - 1 of every
+ * [Hkv][capacity][D] slab; keys encoded from src_pos0.  Any output may be NULL. */
+fcg_status fcg_lib_segment_info(const fcg_lib* lib, int32_t seg_id, int64_t* tok_off,
+                                int32_t* len, int32_t* src_pos0);
+
+/* Device base pointers of layer's K and V slab ([Hkv][capacity][D]). */
+fcg_status fcg_lib_device_ptrs(const fcg_lib* lib, int32_t layer, void** k, void** v);
+
+fcg_status fcg_lib_destroy(fcg_lib* lib);
+
+/* ------------------------------------------------------------------ cache */
+
+/* Create a composite cache for n_seqs sequences of up to max_tokens positions.
+ * page_size == 0: contiguous, one [Hkv][max_tokens][D] region per sequence and
+ * layer (n_pages ignored).  page_size == 16: a pool of n_pages pages per
+ * layer, one page table per sequence shared by all layers; logical page
+ * p / 16 of a sequence is mapped on first write to the lowest-numbered free
+ * page, new pages of one call in ascending (sequence, logical page) order.
+ * With FCG_LAYOUT_ONLY no device memory is allocated and graft, prefill
+ * and decode only validate and record the layout (planning and tests). */
+fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t max_tokens,
+                            int32_t page_size, int32_t n_pages, uint32_t flags, fcg_cache** out);
+
+/* Forget everything written in seq (all layers) and return its pages. */
+fcg_status fcg_cache_reset(fcg_cache* cache, int32_t seq);
+
+/* Host copy of the layout of seq: page_table [ceil(max_tokens / page_size)]
+ * physical page or -1 (paged caches only; may be NULL), *seq_len = 1 + the
+ * highest written position of layer (0 if none; may be NULL), written
+ * [max_tokens] bytes 1/0 per position of layer (may be NULL). */
+fcg_status fcg_cache_export_layout(const fcg_cache* cache, int32_t seq, int32_t layer,
+                                   int32_t* page_table, int32_t* seq_len, uint8_t* written);
+
+/* Device base pointers of layer's K and V region (layouts in the file header). */
+fcg_status fcg_cache_device_ptrs(const fcg_cache* cache, int32_t layer, void** k, void** v);
+
+fcg_status fcg_cache_destroy(fcg_cache* cache);
+
+/* --------------------------------------------------------------- hot path */
+
+/* Cache-stitching (Sec. 4.2, Eq. 4; App. B.1, module-level cache reuse):
+ * for every item i, graft library segment seg[i] into sequence seq[i] at
+ * positions dst[i] .. dst[i] + len - 1, in all layers, keeping its token
+ * order.  Keys are turned by delta = dst[i] - src_pos0 (the rotary encoding of
+ * a key at position p becomes that of p + delta) and rounded to the storage
+ * dtype; values are copied bit for bit.  One launch covers every item and
+ * layer.  seq, seg, dst: host arrays of n_items.
+ * Errors: ERANGE (seq, seg, span outside [0, max_tokens)), EOVERLAP (spans
+ * meet each other or written positions of any layer), ENOMEM (pages), EINVAL
+ * (lib and cache shapes differ, null arrays, a layout-only library with a
+ * cache that has device memory). */
+fcg_status fcg_graft(fcg_cache* cache, const fcg_lib* lib, int32_t n_items, const int32_t* seq,
+                     const int32_t* seg, const int32_t* dst, void* stream);
+
+/* Patch prefill at one layer (Sec. 4.2, Eq. 6; App. B.1, cache-patching):
+ * token t (host seq[t], pos[t]) gets its query and key encoded at pos[t]
+ * (rounded to storage), its key and value stored at pos[t], and
+ * out[t] = softmax(q k^T / sqrt(D)) v over every position <= pos[t] of its
+ * sequence, query head h reading kv head h / (Hq / Hkv).  Tokens may belong to
+ * several sequences and come in any order.  q, k, v, out: device.
+ * Errors: ERANGE, EOVERLAP (position given twice or already written in this
+ * layer), EHOLE (a position below a query's is unwritten after the call),
+ * ENOMEM (pages). */
+fcg_status fcg_patch_prefill(fcg_cache* cache, int32_t layer, int32_t n_tok, const int32_t* seq,
+                             const int32_t* pos, const void* q, const void* k, const void* v,
+                             void* out, void* stream);
+
+/* One decode step at one layer for n_seqs distinct sequences (host seqs):
+ * each appends its token at its current length in that layer and attends
+ * over every position up to it, as in fcg_patch_prefill.  positions_out
+ * (host, may be NULL) receives the positions used.
+ * Errors: EINVAL (duplicate sequence), ERANGE (sequence full), ESTATE
+ * (nothing written in this layer), EHOLE, ENOMEM. */
+fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                      const void* q, const void* k, const void* v, void* out,
+                      int32_t* positions_out, void* stream);
+
+/* ------------------------------------------------------------- diagnostics */
+
+const char* fcg_status_string(fcg_status s);
+const char* fcg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FCG_H */

@@ -40,14 +40,13 @@ def attend_row(q, p: int, K, V, written) -> np.ndarray:
     if not written[:p + 1].all():
         raise ValueError(f"unwritten position below {p}")
     out = np.empty((Hq, D))
-    for hq in range(Hq):
-        h = hq // g
+    for h in range(Hkv):                      # the g query heads of kv head h
         keys = K[:p + 1, h, :]
         vals = V[:p + 1, h, :]
-        s = keys @ q[hq] / np.sqrt(D)
-        e = np.exp(s - s.max())
-        a = e / e.sum()
-        out[hq] = a @ vals
+        s = q[h * g:(h + 1) * g] @ keys.T / np.sqrt(D)          # [g][p + 1]
+        e = np.exp(s - s.max(axis=1, keepdims=True))
+        a = e / e.sum(axis=1, keepdims=True)
+        out[h * g:(h + 1) * g] = a @ vals
     return out
 
 

@@ -1,0 +1,632 @@
+// libfcg C ABI (include/fcg.h): argument checks, the segment library and the
+// composite cache objects, the upload of per-call plans, and kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <deque>
+#include <new>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "fcg.h"
+#include "kernels.hpp"
+#include "planner.hpp"
+
+using namespace fcg;
+
+namespace {
+
+thread_local std::string g_err;
+
+fcg_status fail(fcg_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+fcg_status hip_fail(hipError_t e, const char* what) {
+  return fail(FCG_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+#define HIP_TRY(expr, what)                          \
+  do {                                               \
+    hipError_t e_ = (expr);                          \
+    if (e_ != hipSuccess) return hip_fail(e_, what); \
+  } while (0)
+
+size_t esize(int32_t dtype) { return dtype == FCG_F32 ? 4 : 2; }
+
+fcg_status check_desc(const fcg_model_desc* d) {
+  if (!d) return fail(FCG_EINVAL, "null model descriptor");
+  if (d->n_layers < 1 || d->n_layers > 255) return fail(FCG_EINVAL, "n_layers must be in [1, 255]");
+  if (d->n_kv_heads < 1 || d->n_q_heads < d->n_kv_heads || d->n_q_heads % d->n_kv_heads)
+    return fail(FCG_EINVAL, "n_q_heads must be a positive multiple of n_kv_heads");
+  int g = d->n_q_heads / d->n_kv_heads;
+  if (g != 1 && g != 2 && g != 4 && g != 8 && g != 16) return fail(FCG_EINVAL, "group size must be 1, 2, 4, 8 or 16");
+  if (d->head_dim != 64 && d->head_dim != 128) return fail(FCG_EINVAL, "head_dim must be 64 or 128");
+  if (!(d->rope_theta > 1.0) || !std::isfinite(d->rope_theta)) return fail(FCG_EINVAL, "rope_theta must be > 1");
+  if (d->dtype != FCG_F32 && d->dtype != FCG_BF16) return fail(FCG_EINVAL, "unknown dtype");
+  if (d->rope_style != 0) return fail(FCG_EINVAL, "only rope_style 0 (rotate-half) is supported");
+  return FCG_OK;
+}
+
+bool same_shape(const fcg_model_desc& a, const fcg_model_desc& b) {
+  return a.n_layers == b.n_layers && a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim &&
+         a.dtype == b.dtype && a.rope_theta == b.rope_theta && a.rope_style == b.rope_style;
+}
+
+// float64 rotary frequencies w_i = theta^(-2i/D)
+fcg_status upload_inv_freq(const fcg_model_desc& d, double** out) {
+  std::vector<double> w(d.head_dim / 2);
+  for (int i = 0; i < d.head_dim / 2; ++i) w[i] = std::pow(d.rope_theta, -2.0 * i / d.head_dim);
+  HIP_TRY(hipMalloc(out, w.size() * sizeof(double)), "hipMalloc(inv_freq)");
+  HIP_TRY(hipMemcpy(*out, w.data(), w.size() * sizeof(double), hipMemcpyHostToDevice), "hipMemcpy(inv_freq)");
+  return FCG_OK;
+}
+
+// Staging of per-call plans: a pinned host ring mirrored by a device ring.  A
+// call packs its arrays into one blob, copies it host-to-device on the call's
+// stream and records an event; a region is reused only after its event.
+struct Ring {
+  char* host = nullptr;
+  char* dev = nullptr;
+  size_t cap = 0, head = 0;
+  std::deque<std::tuple<size_t, size_t, hipEvent_t>> inflight;
+  std::vector<hipEvent_t> spare;
+
+  ~Ring() { release(); }
+  void release() {
+    for (auto& f : inflight) {
+      hipEventSynchronize(std::get<2>(f));
+      hipEventDestroy(std::get<2>(f));
+    }
+    inflight.clear();
+    for (auto e : spare) hipEventDestroy(e);
+    spare.clear();
+    if (host) hipHostFree(host);
+    if (dev) hipFree(dev);
+    host = dev = nullptr;
+    cap = head = 0;
+  }
+  fcg_status reserve(size_t n) {
+    if (n <= cap) return FCG_OK;
+    size_t nc = std::max<size_t>(cap * 2, std::max<size_t>(n, 1 << 20));
+    release();
+    HIP_TRY(hipHostMalloc((void**)&host, nc, hipHostMallocDefault), "hipHostMalloc(staging)");
+    HIP_TRY(hipMalloc((void**)&dev, nc), "hipMalloc(staging)");
+    cap = nc;
+    return FCG_OK;
+  }
+  // Region [off, off + n) of both rings, free for writing.
+  fcg_status acquire(size_t n, size_t* off) {
+    fcg_status st = reserve(n);
+    if (st) return st;
+    if (head + n > cap) head = 0;
+    const size_t a = head, b = head + n;
+    for (auto it = inflight.begin(); it != inflight.end();) {
+      if (std::get<1>(*it) <= a || std::get<0>(*it) >= b) {
+        ++it;
+        continue;
+      }
+      HIP_TRY(hipEventSynchronize(std::get<2>(*it)), "hipEventSynchronize(staging)");
+      spare.push_back(std::get<2>(*it));
+      it = inflight.erase(it);
+    }
+    head = b;
+    *off = a;
+    return FCG_OK;
+  }
+  fcg_status retire(size_t off, size_t n, hipStream_t s) {
+    hipEvent_t e;
+    if (!spare.empty()) {
+      e = spare.back();
+      spare.pop_back();
+    } else {
+      HIP_TRY(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate");
+    }
+    HIP_TRY(hipEventRecord(e, s), "hipEventRecord");
+    inflight.emplace_back(off, off + n, e);
+    return FCG_OK;
+  }
+};
+
+// Packs host arrays into one blob with 256-byte aligned members.
+struct Blob {
+  std::vector<char> bytes;
+  size_t add(const void* p, size_t n) {
+    size_t off = (bytes.size() + 255) & ~size_t(255);
+    bytes.resize(off + n);
+    if (n) std::memcpy(bytes.data() + off, p, n);
+    return off;
+  }
+};
+
+}  // namespace
+
+struct Segment {
+  int64_t tok_off;
+  int32_t len, src_pos0;
+};
+
+struct fcg_lib {
+  fcg_model_desc desc;
+  int64_t cap = 0, used = 0;
+  int32_t max_segments = 0;
+  uint32_t flags = 0;
+  std::vector<Segment> segs;
+  void* k = nullptr;
+  void* v = nullptr;
+  int device = 0;
+};
+
+struct fcg_cache {
+  fcg_model_desc desc;
+  int32_t n_seqs, max_tokens, page_size, n_pages;
+  uint32_t flags;
+  Planner plan;
+  void* k = nullptr;
+  void* v = nullptr;
+  int64_t layer_stride = 0;
+  int32_t* d_page_table = nullptr;
+  double* d_inv_freq = nullptr;
+  int device = 0;
+  Ring ring;
+  // workspaces, grown on demand
+  void* qws = nullptr;
+  size_t qws_bytes = 0;
+  float* part = nullptr;
+  size_t part_bytes = 0;
+
+  fcg_cache(const fcg_model_desc& d, int32_t ns, int32_t mt, int32_t ps, int32_t np, uint32_t fl)
+      : desc(d), n_seqs(ns), max_tokens(mt), page_size(ps), n_pages(np), flags(fl),
+        plan(d.n_layers, ns, mt, ps, np) {}
+  bool layout_only() const { return flags & FCG_LAYOUT_ONLY; }
+
+  CacheView view() const {
+    CacheView c;
+    c.k = k;
+    c.v = v;
+    c.layer_stride = layer_stride;
+    c.page_table = d_page_table;
+    c.n_seqs = n_seqs;
+    c.max_tokens = max_tokens;
+    c.page_size = page_size;
+    c.n_lp = plan.n_logical_pages();
+    c.n_kv_heads = desc.n_kv_heads;
+    c.head_dim = desc.head_dim;
+    return c;
+  }
+};
+
+namespace {
+
+fcg_status grow(void** p, size_t* have, size_t need, const char* what) {
+  if (need <= *have) return FCG_OK;
+  if (*p) {
+    HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(grow)");
+    hipFree(*p);
+    *p = nullptr;
+    *have = 0;
+  }
+  size_t n = std::max(need, *have * 2);
+  hipError_t e = hipMalloc(p, n);
+  if (e != hipSuccess) return fail(FCG_ENOMEM, std::string("hipMalloc(") + what + ") failed");
+  *have = n;
+  return FCG_OK;
+}
+
+// After a planner check: map the new pages, and prepare the device copies of
+// the touched page-table rows (appended to the blob).
+void stage_pages(fcg_cache* c, const std::vector<std::pair<int32_t, int32_t>>& new_pages, Blob* blob,
+                 std::vector<std::pair<int32_t, size_t>>* rows) {
+  c->plan.map_pages(new_pages);
+  std::vector<int32_t> seqs;
+  for (auto& sl : new_pages) seqs.push_back(sl.first);
+  std::sort(seqs.begin(), seqs.end());
+  seqs.erase(std::unique(seqs.begin(), seqs.end()), seqs.end());
+  for (int32_t s : seqs)
+    rows->push_back({s, blob->add(c->plan.page_row(s), sizeof(int32_t) * c->plan.n_logical_pages())});
+}
+
+// Upload the blob; copy page rows into the device page table.  *dev receives
+// the device address of the blob.
+fcg_status upload(fcg_cache* c, const Blob& blob, const std::vector<std::pair<int32_t, size_t>>& rows,
+                  hipStream_t s, char** dev, size_t* off_out) {
+  size_t n = std::max<size_t>(blob.bytes.size(), 256), off;
+  fcg_status st = c->ring.acquire(n, &off);
+  if (st) return st;
+  std::memcpy(c->ring.host + off, blob.bytes.data(), blob.bytes.size());
+  HIP_TRY(hipMemcpyAsync(c->ring.dev + off, c->ring.host + off, blob.bytes.size(), hipMemcpyHostToDevice, s),
+          "hipMemcpyAsync(plan)");
+  const size_t nlp = c->plan.n_logical_pages();
+  for (auto& r : rows)
+    HIP_TRY(hipMemcpyAsync(c->d_page_table + (size_t)r.first * nlp, c->ring.dev + off + r.second,
+                           nlp * sizeof(int32_t), hipMemcpyDeviceToDevice, s),
+            "hipMemcpyAsync(page table)");
+  *dev = c->ring.dev + off;
+  *off_out = off;
+  return FCG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fcg_status_string(fcg_status s) {
+  switch (s) {
+    case FCG_OK: return "FCG_OK";
+    case FCG_EINVAL: return "FCG_EINVAL";
+    case FCG_ERANGE: return "FCG_ERANGE";
+    case FCG_EOVERLAP: return "FCG_EOVERLAP";
+    case FCG_EHOLE: return "FCG_EHOLE";
+    case FCG_ENOMEM: return "FCG_ENOMEM";
+    case FCG_ESTATE: return "FCG_ESTATE";
+    case FCG_EHIP: return "FCG_EHIP";
+  }
+  return "FCG_UNKNOWN";
+}
+
+const char* fcg_last_error(void) { return g_err.c_str(); }
+
+// ------------------------------------------------------------------ library
+
+fcg_status fcg_lib_create(const fcg_model_desc* desc, int64_t capacity_tokens, int32_t max_segments, uint32_t flags,
+                          fcg_lib** out) {
+  if (!out) return fail(FCG_EINVAL, "null output handle");
+  if (fcg_status st = check_desc(desc)) return st;
+  if (capacity_tokens < 1 || max_segments < 1) return fail(FCG_EINVAL, "capacity and max_segments must be >= 1");
+  if (flags & ~FCG_LAYOUT_ONLY) return fail(FCG_EINVAL, "unknown flags");
+  fcg_lib* lib = new (std::nothrow) fcg_lib();
+  if (!lib) return fail(FCG_ENOMEM, "host allocation");
+  lib->desc = *desc;
+  lib->cap = capacity_tokens;
+  lib->max_segments = max_segments;
+  lib->flags = flags;
+  if (flags & FCG_LAYOUT_ONLY) {
+    *out = lib;
+    return FCG_OK;
+  }
+  hipGetDevice(&lib->device);
+  const size_t bytes = (size_t)desc->n_layers * desc->n_kv_heads * capacity_tokens * desc->head_dim * esize(desc->dtype);
+  if (hipMalloc(&lib->k, bytes) != hipSuccess || hipMalloc(&lib->v, bytes) != hipSuccess) {
+    if (lib->k) hipFree(lib->k);
+    delete lib;
+    return fail(FCG_ENOMEM, "library slabs do not fit in device memory");
+  }
+  *out = lib;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, const void* k, const void* v,
+                               void* stream, int32_t* seg_id) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (len < 1) return fail(FCG_EINVAL, "segment length must be >= 1");
+  if (src_pos0 < 0) return fail(FCG_ERANGE, "negative source position");
+  if ((k == nullptr) != (v == nullptr)) return fail(FCG_EINVAL, "k and v must both be given or both be null");
+  if (k && (lib->flags & FCG_LAYOUT_ONLY)) return fail(FCG_EINVAL, "a layout-only library takes no data");
+  if ((int32_t)lib->segs.size() >= lib->max_segments) return fail(FCG_ENOMEM, "max_segments reached");
+  if (lib->used + len > lib->cap) return fail(FCG_ENOMEM, "library capacity exhausted");
+  const Segment sg{lib->used, len, src_pos0};
+  if (k) {
+    HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+    const fcg_model_desc& d = lib->desc;
+    int rc = launch_lib_ingest(d.dtype, k, v, lib->k, lib->v, d.n_layers, len, d.n_kv_heads, d.head_dim, lib->cap,
+                               sg.tok_off, (hipStream_t)stream);
+    if (rc) return hip_fail((hipError_t)rc, "ingest launch");
+  }
+  lib->segs.push_back(sg);
+  lib->used += len;
+  if (seg_id) *seg_id = (int32_t)lib->segs.size() - 1;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_segment_info(const fcg_lib* lib, int32_t seg_id, int64_t* tok_off, int32_t* len,
+                                int32_t* src_pos0) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (seg_id < 0 || seg_id >= (int32_t)lib->segs.size()) return fail(FCG_ERANGE, "segment id out of range");
+  const Segment& s = lib->segs[seg_id];
+  if (tok_off) *tok_off = s.tok_off;
+  if (len) *len = s.len;
+  if (src_pos0) *src_pos0 = s.src_pos0;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_device_ptrs(const fcg_lib* lib, int32_t layer, void** k, void** v) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (lib->flags & FCG_LAYOUT_ONLY) return fail(FCG_ESTATE, "layout-only library has no device memory");
+  if (layer < 0 || layer >= lib->desc.n_layers) return fail(FCG_ERANGE, "layer out of range");
+  const size_t off = (size_t)layer * lib->desc.n_kv_heads * lib->cap * lib->desc.head_dim * esize(lib->desc.dtype);
+  if (k) *k = (char*)lib->k + off;
+  if (v) *v = (char*)lib->v + off;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_destroy(fcg_lib* lib) {
+  if (!lib) return FCG_OK;
+  if (lib->flags & FCG_LAYOUT_ONLY) {
+    delete lib;
+    return FCG_OK;
+  }
+  hipSetDevice(lib->device);
+  hipDeviceSynchronize();
+  if (lib->k) hipFree(lib->k);
+  if (lib->v) hipFree(lib->v);
+  delete lib;
+  return FCG_OK;
+}
+
+// -------------------------------------------------------------------- cache
+
+fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t max_tokens, int32_t page_size,
+                            int32_t n_pages, uint32_t flags, fcg_cache** out) {
+  if (!out) return fail(FCG_EINVAL, "null output handle");
+  if (fcg_status st = check_desc(desc)) return st;
+  if (n_seqs < 1 || max_tokens < 1) return fail(FCG_EINVAL, "n_seqs and max_tokens must be >= 1");
+  if (page_size != 0 && page_size != 16) return fail(FCG_EINVAL, "page_size must be 0 (contiguous) or 16");
+  if (page_size && n_pages < 1) return fail(FCG_EINVAL, "a paged cache needs n_pages >= 1");
+  if (flags & ~FCG_LAYOUT_ONLY) return fail(FCG_EINVAL, "unknown flags");
+  fcg_cache* c = new (std::nothrow) fcg_cache(*desc, n_seqs, max_tokens, page_size, page_size ? n_pages : 0, flags);
+  if (!c) return fail(FCG_ENOMEM, "host allocation");
+  if (!c->layout_only()) {
+    hipGetDevice(&c->device);
+    const int64_t per_layer = page_size ? (int64_t)n_pages * desc->n_kv_heads * page_size * desc->head_dim
+                                        : (int64_t)n_seqs * desc->n_kv_heads * max_tokens * desc->head_dim;
+    c->layer_stride = per_layer;
+    const size_t bytes = (size_t)per_layer * desc->n_layers * esize(desc->dtype);
+    bool ok = hipMalloc(&c->k, bytes) == hipSuccess && hipMalloc(&c->v, bytes) == hipSuccess;
+    if (ok && page_size) {
+      const size_t pt = (size_t)n_seqs * c->plan.n_logical_pages() * sizeof(int32_t);
+      ok = hipMalloc((void**)&c->d_page_table, pt) == hipSuccess && hipMemset(c->d_page_table, 0xFF, pt) == hipSuccess;
+    }
+    if (!ok) {
+      fcg_cache_destroy(c);
+      return fail(FCG_ENOMEM, "cache does not fit in device memory");
+    }
+    if (fcg_status st = upload_inv_freq(*desc, &c->d_inv_freq)) {
+      fcg_cache_destroy(c);
+      return st;
+    }
+  }
+  *out = c;
+  return FCG_OK;
+}
+
+fcg_status fcg_cache_reset(fcg_cache* c, int32_t seq) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
+  c->plan.reset(seq);
+  // the device page-table row is rewritten on the next mapping of this
+  // sequence; stale entries are never read because unwritten positions are
+  // never read
+  return FCG_OK;
+}
+
+fcg_status fcg_cache_export_layout(const fcg_cache* c, int32_t seq, int32_t layer, int32_t* page_table,
+                                   int32_t* seq_len, uint8_t* written) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
+  if (layer < 0 || layer >= c->desc.n_layers) return fail(FCG_ERANGE, "layer out of range");
+  if (page_table && c->page_size)
+    std::memcpy(page_table, c->plan.page_row(seq), sizeof(int32_t) * c->plan.n_logical_pages());
+  if (seq_len) *seq_len = c->plan.seq_len(seq, layer);
+  if (written)
+    for (int32_t p = 0; p < c->max_tokens; ++p) written[p] = c->plan.written(seq, layer, p) ? 1 : 0;
+  return FCG_OK;
+}
+
+fcg_status fcg_cache_device_ptrs(const fcg_cache* c, int32_t layer, void** k, void** v) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (c->layout_only()) return fail(FCG_ESTATE, "layout-only cache has no device memory");
+  if (layer < 0 || layer >= c->desc.n_layers) return fail(FCG_ERANGE, "layer out of range");
+  const size_t off = (size_t)layer * c->layer_stride * esize(c->desc.dtype);
+  if (k) *k = (char*)c->k + off;
+  if (v) *v = (char*)c->v + off;
+  return FCG_OK;
+}
+
+fcg_status fcg_cache_destroy(fcg_cache* c) {
+  if (!c) return FCG_OK;
+  if (!c->layout_only()) {
+    hipSetDevice(c->device);
+    hipDeviceSynchronize();
+    c->ring.release();
+    if (c->k) hipFree(c->k);
+    if (c->v) hipFree(c->v);
+    if (c->d_page_table) hipFree(c->d_page_table);
+    if (c->d_inv_freq) hipFree(c->d_inv_freq);
+    if (c->qws) hipFree(c->qws);
+    if (c->part) hipFree(c->part);
+  }
+  delete c;
+  return FCG_OK;
+}
+
+// ----------------------------------------------------------------- hot path
+
+fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const int32_t* seq, const int32_t* seg,
+                     const int32_t* dst, void* stream) {
+  if (!c || !lib) return fail(FCG_EINVAL, "null cache or library");
+  if (n_items < 0) return fail(FCG_EINVAL, "negative item count");
+  if (n_items > 0 && (!seq || !seg || !dst)) return fail(FCG_EINVAL, "null item array");
+  if (!same_shape(c->desc, lib->desc)) return fail(FCG_EINVAL, "library and cache shapes differ");
+  if ((lib->flags & FCG_LAYOUT_ONLY) && !c->layout_only())
+    return fail(FCG_EINVAL, "a layout-only library can only feed a layout-only cache");
+  std::vector<Span> spans(n_items);
+  for (int32_t i = 0; i < n_items; ++i) {
+    if (seg[i] < 0 || seg[i] >= (int32_t)lib->segs.size()) return fail(FCG_ERANGE, "segment id out of range");
+    const Segment& sg = lib->segs[seg[i]];
+    spans[i] = Span{seq[i], seg[i], dst[i], sg.len, dst[i] - sg.src_pos0};
+  }
+  std::vector<std::pair<int32_t, int32_t>> new_pages;
+  std::string msg;
+  if (fcg_status st = c->plan.check_graft(spans, &new_pages, &msg)) return fail(st, msg);
+  if (n_items == 0) return FCG_OK;
+  if (c->layout_only()) {
+    c->plan.map_pages(new_pages);
+    for (auto& s : spans) c->plan.mark_all_layers(s.seq, s.dst, s.len);
+    return FCG_OK;
+  }
+  HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
+  hipStream_t s = (hipStream_t)stream;
+  Blob blob;
+  std::vector<std::pair<int32_t, size_t>> rows;
+  stage_pages(c, new_pages, &blob, &rows);
+  std::vector<GraftChunk> chunks;
+  for (auto& sp : spans) {
+    const Segment& sg = lib->segs[sp.seg];
+    for (int32_t j = 0; j < sp.len; j += kGraftChunk)
+      chunks.push_back(GraftChunk{sg.tok_off + j, sp.dst + j, sp.seq, sp.delta, std::min(kGraftChunk, sp.len - j), 0, 0});
+  }
+  const size_t o_chunks = blob.add(chunks.data(), chunks.size() * sizeof(GraftChunk));
+  char* dev;
+  size_t off;
+  if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  int rc = launch_graft(c->desc.dtype, (const GraftChunk*)(dev + o_chunks), (int)chunks.size(), lib->k, lib->v,
+                        lib->cap, c->view(), c->d_inv_freq, c->desc.n_layers, s);
+  if (rc) return hip_fail((hipError_t)rc, "graft launch");
+  if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
+  for (auto& sp : spans) c->plan.mark_all_layers(sp.seq, sp.dst, sp.len);
+  return FCG_OK;
+}
+
+namespace {
+
+// Attention over the cache for tokens already sorted into TokenMeta ranks.
+// Builds the split plan, uploads it with the page rows, then runs
+// rope_append -> attention -> (combine).
+fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMeta>& meta, bool decode,
+                         const void* q, const void* k, const void* v, void* out,
+                         const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
+  const fcg_model_desc& d = c->desc;
+  const int n = (int)meta.size();
+  const int g = d.n_q_heads / d.n_kv_heads;
+  const bool mfma = !decode && d.dtype == FCG_BF16;
+  // row blocks: consecutive ranks of one sequence, at most 128 query rows (MFMA) or one token
+  const int max_rank = mfma ? std::max(1, 128 / g) : 1;
+  std::vector<std::pair<int, int>> rblocks;  // (rank0, n_rank)
+  for (int r = 0; r < n;) {
+    int u = r;
+    while (u < n && meta[u].seq == meta[r].seq && u - r < max_rank) ++u;
+    rblocks.push_back({r, u - r});
+    r = u;
+  }
+  // split the key range of each row block so that the grid fills the chip
+  const int tile = mfma ? 64 : 256;
+  int64_t total_tiles = 0;
+  for (auto& rb : rblocks) total_tiles += (meta[rb.first + rb.second - 1].pos + tile) / tile;
+  const int64_t target = std::max<int64_t>(1, 512 / d.n_kv_heads);
+  const int min_tiles = mfma ? 2 : 1;
+  const int64_t per = std::max<int64_t>(min_tiles, (total_tiles + target - 1) / target);
+  std::vector<AttnItem> items;
+  std::vector<CombineItem> comb;
+  int n_part = 0;
+  for (auto& rb : rblocks) {
+    const int kend = meta[rb.first + rb.second - 1].pos + 1;
+    const int64_t span = per * tile;
+    const int nsplit = (int)((kend + span - 1) / span);
+    if (nsplit == 1) {
+      items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, 0, kend, -1, 0, 0});
+    } else {
+      comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit});
+      for (int sidx = 0; sidx < nsplit; ++sidx)
+        items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, (int)(sidx * span),
+                                 (int)std::min<int64_t>(kend, (sidx + 1) * span), n_part + sidx, 0, 0});
+      n_part += nsplit;
+    }
+  }
+  const int stride_rows = mfma ? 128 : g;
+  // workspaces first: a failure here leaves the layout untouched
+  const size_t qbytes = (size_t)d.n_kv_heads * n * g * d.head_dim * esize(d.dtype);
+  if (fcg_status st = grow(&c->qws, &c->qws_bytes, qbytes, "query workspace")) return st;
+  const size_t po = (size_t)n_part * d.n_kv_heads * stride_rows * d.head_dim;
+  const size_t pml = (size_t)n_part * d.n_kv_heads * stride_rows * 2;
+  if (n_part)
+    if (fcg_status st = grow((void**)&c->part, &c->part_bytes, (po + pml) * sizeof(float), "split partials")) return st;
+  Blob blob;
+  std::vector<std::pair<int32_t, size_t>> rows;
+  stage_pages(c, new_pages, &blob, &rows);
+  const size_t o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
+  const size_t o_items = blob.add(items.data(), items.size() * sizeof(AttnItem));
+  const size_t o_comb = blob.add(comb.data(), comb.size() * sizeof(CombineItem));
+  char* dev;
+  size_t off;
+  if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  const TokenMeta* dmeta = (const TokenMeta*)(dev + o_meta);
+  const CacheView cv = c->view();
+  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_inv_freq, d.n_q_heads, c->qws, s);
+  if (rc) return hip_fail((hipError_t)rc, "append launch");
+  float* part_o = c->part;
+  float* part_ml = c->part ? c->part + po : nullptr;
+  if (mfma)
+    rc = launch_attn_mfma((const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv, layer,
+                          d.n_q_heads, out, part_o, part_ml, stride_rows, s);
+  else
+    rc = launch_attn_rows(d.dtype, (const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv,
+                          layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
+  if (rc) return hip_fail((hipError_t)rc, "attention launch");
+  if (!comb.empty()) {
+    rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), dmeta, d.n_q_heads,
+                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s);
+    if (rc) return hip_fail((hipError_t)rc, "combine launch");
+  }
+  return c->ring.retire(off, blob.bytes.size(), s);
+}
+
+}  // namespace
+
+fcg_status fcg_patch_prefill(fcg_cache* c, int32_t layer, int32_t n_tok, const int32_t* seq, const int32_t* pos,
+                             const void* q, const void* k, const void* v, void* out, void* stream) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (n_tok < 0) return fail(FCG_EINVAL, "negative token count");
+  if (n_tok > 0 && (!seq || !pos)) return fail(FCG_EINVAL, "null token array");
+  if (n_tok > 0 && !c->layout_only() && (!q || !k || !v || !out)) return fail(FCG_EINVAL, "null tensor");
+  std::vector<std::pair<int32_t, int32_t>> new_pages;
+  std::string msg;
+  if (fcg_status st = c->plan.check_append(layer, n_tok, seq, pos, &new_pages, &msg)) return fail(st, msg);
+  if (n_tok == 0) return FCG_OK;
+  if (c->layout_only()) {
+    c->plan.map_pages(new_pages);
+    for (int32_t t = 0; t < n_tok; ++t) c->plan.mark(seq[t], layer, pos[t]);
+    return FCG_OK;
+  }
+  HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
+  std::vector<TokenMeta> meta(n_tok);
+  for (int32_t t = 0; t < n_tok; ++t) meta[t] = TokenMeta{t, seq[t], pos[t], 0};
+  std::sort(meta.begin(), meta.end(), [](const TokenMeta& a, const TokenMeta& b) {
+    return a.seq != b.seq ? a.seq < b.seq : a.pos < b.pos;
+  });
+  if (fcg_status st = run_attention(c, layer, meta, false, q, k, v, out, new_pages, (hipStream_t)stream)) return st;
+  for (int32_t t = 0; t < n_tok; ++t) c->plan.mark(seq[t], layer, pos[t]);
+  return FCG_OK;
+}
+
+fcg_status fcg_decode(fcg_cache* c, int32_t layer, int32_t n_seqs, const int32_t* seqs, const void* q,
+                      const void* k, const void* v, void* out, int32_t* positions_out, void* stream) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (n_seqs < 0) return fail(FCG_EINVAL, "negative sequence count");
+  if (n_seqs > 0 && !seqs) return fail(FCG_EINVAL, "null sequence array");
+  if (n_seqs > 0 && !c->layout_only() && (!q || !k || !v || !out)) return fail(FCG_EINVAL, "null tensor");
+  std::vector<int32_t> pos;
+  std::vector<std::pair<int32_t, int32_t>> new_pages;
+  std::string msg;
+  if (fcg_status st = c->plan.check_decode(layer, n_seqs, seqs, &pos, &new_pages, &msg)) return fail(st, msg);
+  if (n_seqs == 0) return FCG_OK;
+  if (!c->layout_only()) {
+    HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
+    std::vector<TokenMeta> meta(n_seqs);
+    for (int32_t i = 0; i < n_seqs; ++i) meta[i] = TokenMeta{i, seqs[i], pos[i], 0};
+    if (fcg_status st = run_attention(c, layer, meta, true, q, k, v, out, new_pages, (hipStream_t)stream)) return st;
+  } else {
+    c->plan.map_pages(new_pages);
+  }
+  for (int32_t i = 0; i < n_seqs; ++i) {
+    c->plan.mark(seqs[i], layer, pos[i]);
+    if (positions_out) positions_out[i] = pos[i];
+  }
+  return FCG_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// Device helpers shared by the gfx950 kernels of libfcg: storage-dtype
+// conversion, 16-byte vector access, rotary angles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fcg {
+
+typedef uint16_t bf16_t;  // raw bfloat16 bits
+
+// bf16 -> fp32 is exact: the bits are the high half of the binary32 pattern.
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float((uint32_t)b << 16); }
+
+// fp32 -> bf16, round to nearest, ties to even (inputs are finite).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// Two fp32 -> packed pair of bf16 (lo in bits 0..15).
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return (uint32_t)f32_to_bf16(lo) | ((uint32_t)f32_to_bf16(hi) << 16);
+}
+
+__device__ __forceinline__ float lo_bf16(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float hi_bf16(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// Storage traits: a 16-byte vector holds VEC elements.
+template <typename T> struct Store;
+template <> struct Store<float> {
+  static constexpr int VEC = 4;
+  __device__ static inline void unpack(const uint4& w, float* x) {
+    x[0] = __uint_as_float(w.x); x[1] = __uint_as_float(w.y);
+    x[2] = __uint_as_float(w.z); x[3] = __uint_as_float(w.w);
+  }
+  __device__ static inline uint4 pack(const float* x) {
+    return make_uint4(__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]), __float_as_uint(x[3]));
+  }
+  __device__ static inline float load1(const float* p) { return *p; }
+  __device__ static inline float round(float x) { return x; }
+  __device__ static inline void store1(float* p, float x) { *p = x; }
+};
+template <> struct Store<bf16_t> {
+  static constexpr int VEC = 8;
+  __device__ static inline void unpack(const uint4& w, float* x) {
+    x[0] = lo_bf16(w.x); x[1] = hi_bf16(w.x); x[2] = lo_bf16(w.y); x[3] = hi_bf16(w.y);
+    x[4] = lo_bf16(w.z); x[5] = hi_bf16(w.z); x[6] = lo_bf16(w.w); x[7] = hi_bf16(w.w);
+  }
+  __device__ static inline uint4 pack(const float* x) {
+    return make_uint4(pack_bf16x2(x[0], x[1]), pack_bf16x2(x[2], x[3]), pack_bf16x2(x[4], x[5]),
+                      pack_bf16x2(x[6], x[7]));
+  }
+  __device__ static inline float load1(const bf16_t* p) { return bf16_to_f32(*p); }
+  __device__ static inline float round(float x) { return bf16_to_f32(f32_to_bf16(x)); }
+  __device__ static inline void store1(bf16_t* p, float x) { *p = f32_to_bf16(x); }
+};
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+__device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
+
+// cos and sin of pos * w for the rotary pair with float64 frequency w: the
+// angle is the float64 product and the float64 cos/sin are rounded to fp32.
+__device__ __forceinline__ void rope_cs(double pos, double w, float* c, float* s) {
+  double sd, cd;
+  sincos(pos * w, &sd, &cd);
+  *c = (float)cd;
+  *s = (float)sd;
+}
+
+}  // namespace fcg

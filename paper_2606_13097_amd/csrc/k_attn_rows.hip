@@ -1,0 +1,232 @@
+// Vector-ALU attention for gfx950: one query token (its g query heads sharing
+// one kv head) per block, over one split [k0, k1) of its causal key range.
+// Used for decode steps (one query per sequence: HBM-bound, about 4 FLOP per
+// byte at g = 4, so matrix cores would idle) and for fp32 caches.
+//
+// Lane layout: a key row of D elements is split into 16-byte vectors; LPK =
+// D / VEC lanes hold one key, so a wave covers 64 / LPK keys per step and
+// every load is a coalesced 16-byte vector.  Scores are reduced across the LPK
+// lanes of a key with DPP (quad_perm, row_half_mirror, row_mirror).  Each lane
+// keeps its own running max / sum / output (online softmax in base 2: the
+// query is pre-scaled by log2(e) / sqrt(D)); the 256 lanes are merged through
+// LDS at the end of the block.  A block that covers the whole range writes the
+// normalised output; otherwise it writes a partial (max, sum, unnormalised
+// output) that the combine kernel merges.
+#include "fcg_device.hpp"
+#include "kernels.hpp"
+
+namespace fcg {
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over groups of LPK consecutive lanes (LPK in 1, 2, 4, 8, 16); every lane gets the sum.
+template <int LPK>
+__device__ __forceinline__ float group_sum(float x) {
+  if (LPK >= 2) x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  if (LPK >= 4) x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  if (LPK >= 8) x += dpp<0x141>(x);  // row_half_mirror
+  if (LPK >= 16) x += dpp<0x140>(x); // row_mirror
+  return x;
+}
+
+template <typename T, int D, int G>
+__global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restrict__ items,
+                                                        const TokenMeta* __restrict__ meta,
+                                                        const T* __restrict__ qws, int rows_ws, CacheView cv,
+                                                        int layer, int Hq, T* __restrict__ out,
+                                                        float* __restrict__ part_o, float* __restrict__ part_ml,
+                                                        int part_stride_rows) {
+  constexpr int VEC = Store<T>::VEC;
+  constexpr int NV = (D / VEC > 16) ? (D / VEC) / 16 : 1;  // 16-byte vectors per lane
+  constexpr int DPL = VEC * NV;                              // dims per lane
+  constexpr int LPK = D / DPL;                               // lanes per key (<= 16)
+  constexpr int SLOTS = 256 / LPK;                           // keys per block step
+  static_assert(LPK <= 16, "a key must fit one DPP row");
+  __shared__ float s_m[SLOTS][G], s_l[SLOTS][G];
+  __shared__ float s_o[SLOTS][DPL][LPK];
+  __shared__ float s_M[G], s_L[G];
+
+  const AttnItem it = items[blockIdx.x];
+  const int hk = blockIdx.y;
+  const int Hkv = cv.n_kv_heads;
+  const TokenMeta m = meta[it.rank0];
+  const int t = threadIdx.x;
+  const int chunk = t % LPK;
+  const int slot = t / LPK;
+  const float qscale = 1.4426950408889634f / sqrtf((float)D);
+
+  float q[G][DPL];
+#pragma unroll
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int nv = 0; nv < NV; ++nv) {
+      float x[VEC];
+      Store<T>::unpack(
+          ld16(qws + ((int64_t)hk * rows_ws + (int64_t)it.rank0 * G + j) * D + chunk * DPL + nv * VEC), x);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) q[j][nv * VEC + e] = x[e] * qscale;
+    }
+  float mx[G], sum[G], o[G][DPL];
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    mx[j] = -INFINITY;
+    sum[j] = 0.f;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o[j][e] = 0.f;
+  }
+  const T* ck = reinterpret_cast<const T*>(cv.k);
+  const T* cvv = reinterpret_cast<const T*>(cv.v);
+  const int end = min(it.k1, m.pos + 1);
+  for (int base = it.k0; base < end; base += SLOTS) {
+    const int key = base + slot;
+    if (key < end) {  // uniform across the LPK lanes of a key, so DPP partners are active
+      const int64_t off = cache_offset(cv, layer, m.seq, hk, key) + chunk * DPL;
+      float kx[DPL], vx[DPL];
+#pragma unroll
+      for (int nv = 0; nv < NV; ++nv) {
+        Store<T>::unpack(ld16(ck + off + nv * VEC), kx + nv * VEC);
+        Store<T>::unpack(ld16(cvv + off + nv * VEC), vx + nv * VEC);
+      }
+      float s[G];
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) a = fmaf(q[j][e], kx[e], a);
+        s[j] = group_sum<LPK>(a);
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float mn = fmaxf(mx[j], s[j]);
+        const float a = exp2f(mx[j] - mn);  // mx = -inf before the first key: a = 0
+        const float p = exp2f(s[j] - mn);
+        sum[j] = fmaf(sum[j], a, p);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) o[j][e] = fmaf(o[j][e], a, p * vx[e]);
+        mx[j] = mn;
+      }
+    }
+  }
+  // merge the SLOTS key slots of the block
+  if (chunk == 0) {
+#pragma unroll
+    for (int j = 0; j < G; ++j) { s_m[slot][j] = mx[j]; s_l[slot][j] = sum[j]; }
+  }
+  __syncthreads();
+  if (t < G) {
+    float M = -INFINITY;
+    for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][t]);
+    float L = 0.f;
+    if (M != -INFINITY)
+      for (int s2 = 0; s2 < SLOTS; ++s2)
+        if (s_m[s2][t] != -INFINITY) L += s_l[s2][t] * exp2f(s_m[s2][t] - M);
+    s_M[t] = M;
+    s_L[t] = L;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const float M = s_M[j];
+    const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : exp2f(mx[j] - M);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) s_o[slot][e][chunk] = o[j][e] * f;
+    __syncthreads();
+    for (int d = t; d < D; d += 256) {
+      const int c = d / DPL, e = d % DPL;
+      float acc = 0.f;
+      for (int s2 = 0; s2 < SLOTS; ++s2) acc += s_o[s2][e][c];
+      if (it.part < 0) {
+        const float L = s_L[j];
+        Store<T>::store1(out + ((int64_t)m.tok * Hq + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
+      } else {
+        const int64_t row = ((int64_t)it.part * Hkv + hk) * part_stride_rows + j;
+        part_o[row * D + d] = acc;
+        if (d == 0) {
+          part_ml[row * 2 + 0] = s_M[j];
+          part_ml[row * 2 + 1] = s_L[j];
+        }
+      }
+    }
+    __syncthreads();
+  }
+}
+
+// Merge split-KV partials: per row, M = max M_s, L = sum L_s 2^(M_s - M),
+// O = sum O_s 2^(M_s - M) / L.  One block per (row block, kv head).
+template <typename T>
+__global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restrict__ items,
+                                                      const TokenMeta* __restrict__ meta, int Hq, int Hkv, int D,
+                                                      const float* __restrict__ part_o,
+                                                      const float* __restrict__ part_ml, int part_stride_rows,
+                                                      T* __restrict__ out) {
+  const CombineItem it = items[blockIdx.x];
+  const int hk = blockIdx.y;
+  const int g = Hq / Hkv;
+  const int rows = it.n_rank * g;
+  for (int i = threadIdx.x; i < rows * D; i += blockDim.x) {
+    const int row = i / D, d = i % D;
+    float M = -INFINITY;
+    for (int s = 0; s < it.n_part; ++s) {
+      const int64_t pr = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + row;
+      M = fmaxf(M, part_ml[pr * 2]);
+    }
+    float L = 0.f, O = 0.f;
+    if (M != -INFINITY)
+      for (int s = 0; s < it.n_part; ++s) {
+        const int64_t pr = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + row;
+        const float ms = part_ml[pr * 2];
+        if (ms == -INFINITY) continue;
+        const float f = exp2f(ms - M);
+        L = fmaf(part_ml[pr * 2 + 1], f, L);
+        O = fmaf(part_o[pr * D + d], f, O);
+      }
+    const TokenMeta m = meta[it.rank0 + row / g];
+    Store<T>::store1(out + ((int64_t)m.tok * Hq + hk * g + row % g) * D + d, L > 0.f ? O / L : 0.f);
+  }
+}
+
+int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
+                     int rows_ws, const CacheView& cv, int layer, int Hq, void* out, float* part_o,
+                     float* part_ml, int part_stride_rows, hipStream_t s) {
+  if (n_items == 0) return 0;
+  const int g = Hq / cv.n_kv_heads;
+  dim3 grid(n_items, cv.n_kv_heads);
+#define AR(T, DD, GG)                                                                                       \
+  hipLaunchKernelGGL((attn_rows_kernel<T, DD, GG>), grid, dim3(256), 0, s, items, meta, (const T*)qws,      \
+                     rows_ws, cv, layer, Hq, (T*)out, part_o, part_ml, part_stride_rows)
+#define ARG(T, DD)                                                                                          \
+  switch (g) {                                                                                              \
+    case 1: AR(T, DD, 1); break;                                                                            \
+    case 2: AR(T, DD, 2); break;                                                                            \
+    case 4: AR(T, DD, 4); break;                                                                            \
+    case 8: AR(T, DD, 8); break;                                                                            \
+    case 16: AR(T, DD, 16); break;                                                                          \
+    default: return -1;                                                                                     \
+  }
+  if (dtype == 0) { if (cv.head_dim == 64) { ARG(float, 64) } else { ARG(float, 128) } }
+  else { if (cv.head_dim == 64) { ARG(bf16_t, 64) } else { ARG(bf16_t, 128) } }
+#undef ARG
+#undef AR
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : (int)e;
+}
+
+int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq, int Hkv,
+                   int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
+                   hipStream_t s) {
+  if (n_items == 0) return 0;
+  dim3 grid(n_items, Hkv);
+  if (dtype == 0)
+    hipLaunchKernelGGL((combine_kernel<float>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, D, part_o, part_ml,
+                       part_stride_rows, (float*)out);
+  else
+    hipLaunchKernelGGL((combine_kernel<bf16_t>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, D, part_o,
+                       part_ml, part_stride_rows, (bf16_t*)out);
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : (int)e;
+}
+
+}  // namespace fcg

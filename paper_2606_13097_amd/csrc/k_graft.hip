@@ -1,0 +1,152 @@
+// Cache-stitching kernels for gfx950 (Sec. 4.2, Eq. 4; App. B.1).
+//
+// graft: every grafted token's key is turned from its source position to its
+// target position (a rotation by the segment's delta, rotate-half pairs
+// (i, i + D/2), angle delta * theta^(-2i/D)) and its value is copied.  The
+// kernel is a pure HBM stream: each lane moves whole 16-byte vectors, the two
+// halves of a rotary pair are loaded by the same lane, all loads of a block are
+// issued before its stores, and data never passes through LDS (LDS holds only
+// the D/2 cos/sin values of the block's delta, computed once per block).
+//
+// ingest: copy a segment given token-major [L][len][Hkv][D] into the library's
+// head-major slabs [L][Hkv][cap][D].
+#include "fcg_device.hpp"
+#include "kernels.hpp"
+
+namespace fcg {
+
+template <typename T, int D>
+__global__ void __launch_bounds__(256) ingest_kernel(const T* __restrict__ k, const T* __restrict__ v,
+                                                     T* __restrict__ lk, T* __restrict__ lv, int len, int Hkv,
+                                                     int64_t cap, int64_t tok_off) {
+  constexpr int VEC = Store<T>::VEC;
+  constexpr int VPR = D / VEC;  // vectors per (token, head) row
+  const int l = blockIdx.y;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = (int64_t)len * Hkv * VPR;
+  if (i >= n) return;
+  const int c = (int)(i % VPR);
+  const int64_t th = i / VPR;
+  const int h = (int)(th % Hkv);
+  const int64_t j = th / Hkv;
+  const int64_t src = (((int64_t)l * len + j) * Hkv + h) * D + c * VEC;
+  const int64_t dst = (((int64_t)l * Hkv + h) * cap + tok_off + j) * D + c * VEC;
+  st16(lk + dst, ld16(k + src));
+  st16(lv + dst, ld16(v + src));
+}
+
+template <typename T, int D, bool PAGED>
+__global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict__ chunks,
+                                                    const T* __restrict__ lib_k, const T* __restrict__ lib_v,
+                                                    int64_t cap, CacheView cv, const double* __restrict__ inv_freq) {
+  constexpr int VEC = Store<T>::VEC;
+  constexpr int HALF = D / 2;
+  constexpr int KT = HALF / VEC;            // lanes per key row (each owns a pair of vectors)
+  constexpr int KR = 256 / KT;              // key rows per pass
+  constexpr int KP = (kGraftChunk + KR - 1) / KR;
+  constexpr int VT = D / VEC;               // lanes per value row
+  constexpr int VR = 256 / VT;
+  constexpr int VP = (kGraftChunk + VR - 1) / VR;
+
+  __shared__ float s_cos[HALF], s_sin[HALF];
+
+  const GraftChunk ch = chunks[blockIdx.x];
+  const int h = blockIdx.y;
+  const int l = blockIdx.z;
+  const int t = threadIdx.x;
+  const int Hkv = cv.n_kv_heads;
+
+  if (t < HALF) rope_cs((double)ch.delta, inv_freq[t], &s_cos[t], &s_sin[t]);
+
+  const int64_t src_base = (((int64_t)l * Hkv + h) * cap + ch.src_tok) * D;
+  const T* sk = lib_k + src_base;
+  const T* sv = lib_v + src_base;
+  T* ck = reinterpret_cast<T*>(cv.k);
+  T* cvv = reinterpret_cast<T*>(cv.v);
+
+  // issue every load of the block first
+  uint4 klo[KP], khi[KP], vv[VP];
+  const int kc = t % KT, kr = t / KT;
+#pragma unroll
+  for (int p = 0; p < KP; ++p) {
+    const int j = p * KR + kr;
+    if (j < ch.n) {
+      klo[p] = ld16(sk + (int64_t)j * D + kc * VEC);
+      khi[p] = ld16(sk + (int64_t)j * D + HALF + kc * VEC);
+    }
+  }
+  const int vc = t % VT, vr = t / VT;
+#pragma unroll
+  for (int p = 0; p < VP; ++p) {
+    const int j = p * VR + vr;
+    if (j < ch.n) vv[p] = ld16(sv + (int64_t)j * D + vc * VEC);
+  }
+  __syncthreads();  // cos/sin ready
+
+  float c[VEC], s[VEC];
+#pragma unroll
+  for (int e = 0; e < VEC; ++e) {
+    c[e] = s_cos[kc * VEC + e];
+    s[e] = s_sin[kc * VEC + e];
+  }
+#pragma unroll
+  for (int p = 0; p < KP; ++p) {
+    const int j = p * KR + kr;
+    if (j < ch.n) {
+      float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
+      Store<T>::unpack(klo[p], x1);
+      Store<T>::unpack(khi[p], x2);
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) {
+        y1[e] = fmaf(x1[e], c[e], -x2[e] * s[e]);
+        y2[e] = fmaf(x2[e], c[e], x1[e] * s[e]);
+      }
+      const int64_t off = cache_offset(cv, l, ch.seq, h, ch.dst + j);
+      st16(ck + off + kc * VEC, Store<T>::pack(y1));
+      st16(ck + off + HALF + kc * VEC, Store<T>::pack(y2));
+    }
+  }
+#pragma unroll
+  for (int p = 0; p < VP; ++p) {
+    const int j = p * VR + vr;
+    if (j < ch.n) {
+      const int64_t off = cache_offset(cv, l, ch.seq, h, ch.dst + j);
+      st16(cvv + off + vc * VEC, vv[p]);
+    }
+  }
+}
+
+static int check(hipError_t e) { return e == hipSuccess ? 0 : (int)e; }
+
+int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len, int Hkv,
+                      int D, int64_t cap, int64_t tok_off, hipStream_t s) {
+  const int vec = dtype == 0 ? 4 : 8;
+  const int64_t n = (int64_t)len * Hkv * (D / vec);
+  if (n == 0) return 0;
+  dim3 grid((unsigned)((n + 255) / 256), L);
+#define ING(T, DD)                                                                                          \
+  hipLaunchKernelGGL((ingest_kernel<T, DD>), grid, dim3(256), 0, s, (const T*)k, (const T*)v, (T*)lib_k,    \
+                     (T*)lib_v, len, Hkv, cap, tok_off)
+  if (dtype == 0) { if (D == 64) ING(float, 64); else ING(float, 128); }
+  else { if (D == 64) ING(bf16_t, 64); else ING(bf16_t, 128); }
+#undef ING
+  return check(hipGetLastError());
+}
+
+int launch_graft(int dtype, const GraftChunk* chunks, int n_chunks, const void* lib_k, const void* lib_v,
+                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s) {
+  if (n_chunks == 0) return 0;
+  dim3 grid(n_chunks, cv.n_kv_heads, L);
+#define GR(T, DD, PG)                                                                                       \
+  hipLaunchKernelGGL((graft_kernel<T, DD, PG>), grid, dim3(256), 0, s, chunks, (const T*)lib_k,             \
+                     (const T*)lib_v, cap, cv, inv_freq)
+#define GRD(T, PG) { if (cv.head_dim == 64) GR(T, 64, PG); else GR(T, 128, PG); }
+  const bool paged = cv.page_size != 0;
+  if (dtype == 0) { if (paged) GRD(float, true) else GRD(float, false) }
+  else { if (paged) GRD(bf16_t, true) else GRD(bf16_t, false) }
+#undef GRD
+#undef GR
+  return check(hipGetLastError());
+}
+
+}  // namespace fcg

@@ -1,0 +1,92 @@
+// Launch interface between the host side of libfcg (api.cpp) and its gfx950
+// kernels.  Plain structs and pointers only.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fcg {
+
+// One run of up to kGraftChunk tokens of one grafted segment.
+struct GraftChunk {
+  int64_t src_tok;  // token index in the library slab of the first token
+  int32_t dst;      // target position of the first token
+  int32_t seq;      // target sequence
+  int32_t delta;    // rotary turn of the keys (dst - src_pos0 of the segment)
+  int32_t n;        // tokens in this run
+  int32_t pad0, pad1;
+};
+constexpr int kGraftChunk = 64;
+
+// Device view of a composite cache (all layers).
+struct CacheView {
+  void* k;               // layer-0 base of K
+  void* v;               // layer-0 base of V
+  int64_t layer_stride;  // elements from one layer's region to the next
+  const int32_t* page_table;  // device [n_seqs][n_lp] (paged only)
+  int32_t n_seqs, max_tokens, page_size, n_lp;
+  int32_t n_kv_heads, head_dim;
+};
+
+// Offset (elements) of (layer, seq, head, pos) inside a cache; page_size is 0
+// (contiguous) or a power of two.
+__host__ __device__ inline int64_t cache_offset(const CacheView& c, int layer, int seq, int head, int pos) {
+  int64_t base = (int64_t)layer * c.layer_stride;
+  if (c.page_size == 0)
+    return base + (((int64_t)seq * c.n_kv_heads + head) * c.max_tokens + pos) * c.head_dim;
+  int32_t page = c.page_table[(int64_t)seq * c.n_lp + pos / c.page_size];
+  return base + (((int64_t)page * c.n_kv_heads + head) * c.page_size + (pos % c.page_size)) * c.head_dim;
+}
+
+// Per fresh (or decode) token, in attention order: tokens grouped by sequence,
+// ascending position inside a sequence.  Query rows of kv head h for the token
+// of rank r are r * g .. r * g + g - 1 of the query workspace.
+struct TokenMeta {
+  int32_t tok;  // index of the token in the caller's q/k/v/out arrays
+  int32_t seq;
+  int32_t pos;
+  int32_t pad;
+};
+
+// A block of consecutive ranks (one sequence) attended over keys [k0, k1).
+struct AttnItem {
+  int32_t rank0, n_rank;  // token ranks of the row block
+  int32_t seq;
+  int32_t k0, k1;         // key positions of this split
+  int32_t part;           // partial-result slot (-1: the only split, write the output directly)
+  int32_t pad0, pad1;
+};
+
+// Row block -> its partial slots, for the split-KV combine.
+struct CombineItem {
+  int32_t rank0, n_rank;
+  int32_t part0, n_part;  // partial slots part0 .. part0 + n_part - 1
+};
+
+int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len,
+                      int Hkv, int D, int64_t cap, int64_t tok_off, hipStream_t s);
+
+int launch_graft(int dtype, const GraftChunk* chunks, int n_chunks, const void* lib_k, const void* lib_v,
+                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s);
+
+// Encode q and k of n tokens at their positions, store k and v in the cache
+// (layer), write encoded q to qws [Hkv][n * g][D].
+int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, const void* k, const void* v,
+                       const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws,
+                       hipStream_t s);
+
+// bf16 MFMA attention of query-workspace rows over the cache.
+int launch_attn_mfma(const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws, int rows_ws,
+                     const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
+                     int part_stride_rows, hipStream_t s);
+
+// VALU attention, one token (g query rows) per item; any dtype.
+int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
+                     int rows_ws, const CacheView& cv, int layer, int Hq, void* out, float* part_o,
+                     float* part_ml, int part_stride_rows, hipStream_t s);
+
+int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
+                   int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
+                   hipStream_t s);
+
+}  // namespace fcg

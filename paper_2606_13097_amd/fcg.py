@@ -1,0 +1,253 @@
+"""Thin Python binding of libfcg.so (C ABI in include/fcg.h).
+
+Argument marshalling only: every step of the grafting path runs in the HIP
+kernels of libfcg.so.  Functions carry the C names.  Device tensors are torch
+tensors on the GPU (only their ``data_ptr`` is passed); host index arrays are
+anything ``numpy.asarray(..., int32)`` accepts.  A failing call raises
+``FcgError`` with the status and the library's message.
+
+If libfcg.so is missing this module raises at import: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+# PyTorch ships its own libamdhip64 (soname libamdhip64.so.7).  Loading torch
+# first makes the dynamic linker bind libfcg.so to that same runtime, so
+# torch's streams and allocations and libfcg's kernels share one HIP runtime.
+import torch  # noqa: F401
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfcg.so")
+
+FCG_F32, FCG_BF16 = 0, 1
+FCG_LAYOUT_ONLY = 1
+STATUS = ["FCG_OK", "FCG_EINVAL", "FCG_ERANGE", "FCG_EOVERLAP", "FCG_EHOLE", "FCG_ENOMEM", "FCG_ESTATE",
+          "FCG_EHIP"]
+FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE, FCG_EHIP = range(8)
+
+# every symbol include/fcg.h declares
+EXPORTS = [
+    "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
+    "fcg_cache_create", "fcg_cache_reset", "fcg_cache_export_layout", "fcg_cache_device_ptrs",
+    "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
+]
+
+
+class FcgError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS[status] if 0 <= status < len(STATUS) else status}: {msg}")
+        self.status = status
+
+
+class ModelDesc(C.Structure):
+    _fields_ = [("n_layers", C.c_int32), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("rope_theta", C.c_double), ("dtype", C.c_int32),
+                ("rope_style", C.c_int32)]
+
+
+def model_desc(n_layers, n_q_heads, n_kv_heads, head_dim, rope_theta, dtype) -> ModelDesc:
+    dt = {"f32": FCG_F32, "bf16": FCG_BF16}.get(dtype, dtype)
+    return ModelDesc(n_layers, n_q_heads, n_kv_heads, head_dim, float(rope_theta), int(dt), 0)
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_13097_amd.build`")
+    lib = C.CDLL(LIB_PATH)
+    P, I32, I64, U32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32
+    PI32, PI64, PU8 = C.POINTER(C.c_int32), C.POINTER(C.c_int64), C.POINTER(C.c_uint8)
+    sig = {
+        "fcg_lib_create": [C.POINTER(ModelDesc), I64, I32, U32, C.POINTER(P)],
+        "fcg_lib_add_segment": [P, I32, I32, P, P, P, PI32],
+        "fcg_lib_segment_info": [P, I32, PI64, PI32, PI32],
+        "fcg_lib_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
+        "fcg_lib_destroy": [P],
+        "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
+        "fcg_cache_reset": [P, I32],
+        "fcg_cache_export_layout": [P, I32, I32, PI32, PI32, PU8],
+        "fcg_cache_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
+        "fcg_cache_destroy": [P],
+        "fcg_graft": [P, P, I32, PI32, PI32, PI32, P],
+        "fcg_patch_prefill": [P, I32, I32, PI32, PI32, P, P, P, P, P],
+        "fcg_decode": [P, I32, I32, PI32, P, P, P, P, PI32, P],
+    }
+    for name, args in sig.items():
+        f = getattr(lib, name)
+        f.argtypes = args
+        f.restype = C.c_int
+    lib.fcg_status_string.argtypes = [C.c_int]
+    lib.fcg_status_string.restype = C.c_char_p
+    lib.fcg_last_error.argtypes = []
+    lib.fcg_last_error.restype = C.c_char_p
+    return lib
+
+
+_L = _load()
+
+
+def _check(status: int) -> None:
+    if status != FCG_OK:
+        raise FcgError(status, _L.fcg_last_error().decode())
+
+
+def _i32(a) -> np.ndarray:
+    return np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+
+
+def _p(a: np.ndarray):
+    return a.ctypes.data_as(C.POINTER(C.c_int32)) if a.size else None
+
+
+def _dptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        try:
+            import torch
+            if torch.cuda.is_available():
+                return torch.cuda.current_stream().cuda_stream
+        except Exception:
+            pass
+        return None
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+class Library:
+    """Handle of a segment library (``fcg_lib``)."""
+
+    h = None
+
+    def __init__(self, desc: ModelDesc, capacity_tokens: int, max_segments: int, flags: int = 0):
+        h = C.c_void_p()
+        _check(_L.fcg_lib_create(C.byref(desc), int(capacity_tokens), int(max_segments), int(flags), C.byref(h)))
+        self.h, self.desc = h, desc
+        self.capacity = int(capacity_tokens)
+
+    def close(self):
+        if self.h:
+            _L.fcg_lib_destroy(self.h)
+            self.h = None
+
+    __del__ = close
+
+
+class Cache:
+    """Handle of a composite cache (``fcg_cache``)."""
+
+    h = None
+
+    def __init__(self, desc: ModelDesc, n_seqs: int, max_tokens: int, page_size: int = 0, n_pages: int = 0,
+                 flags: int = 0):
+        h = C.c_void_p()
+        _check(_L.fcg_cache_create(C.byref(desc), int(n_seqs), int(max_tokens), int(page_size), int(n_pages),
+                                   int(flags), C.byref(h)))
+        self.h, self.desc = h, desc
+        self.n_seqs, self.max_tokens, self.page_size, self.n_pages = n_seqs, max_tokens, page_size, n_pages
+        self.n_lp = -(-max_tokens // page_size) if page_size else 0
+
+    def close(self):
+        if self.h:
+            _L.fcg_cache_destroy(self.h)
+            self.h = None
+
+    __del__ = close
+
+
+def fcg_lib_create(desc: ModelDesc, capacity_tokens: int, max_segments: int, flags: int = 0) -> Library:
+    return Library(desc, capacity_tokens, max_segments, flags)
+
+
+def fcg_lib_add_segment(lib: Library, length: int, src_pos0: int, k=None, v=None, stream=None) -> int:
+    sid = C.c_int32()
+    _check(_L.fcg_lib_add_segment(lib.h, int(length), int(src_pos0), _dptr(k), _dptr(v),
+                                  _stream(stream) if k is not None else None, C.byref(sid)))
+    return sid.value
+
+
+def fcg_lib_segment_info(lib: Library, seg_id: int):
+    off, n, src = C.c_int64(), C.c_int32(), C.c_int32()
+    _check(_L.fcg_lib_segment_info(lib.h, int(seg_id), C.byref(off), C.byref(n), C.byref(src)))
+    return off.value, n.value, src.value
+
+
+def fcg_lib_device_ptrs(lib: Library, layer: int):
+    k, v = C.c_void_p(), C.c_void_p()
+    _check(_L.fcg_lib_device_ptrs(lib.h, int(layer), C.byref(k), C.byref(v)))
+    return k.value, v.value
+
+
+def fcg_lib_destroy(lib: Library) -> None:
+    lib.close()
+
+
+def fcg_cache_create(desc: ModelDesc, n_seqs: int, max_tokens: int, page_size: int = 0, n_pages: int = 0,
+                     flags: int = 0) -> Cache:
+    return Cache(desc, n_seqs, max_tokens, page_size, n_pages, flags)
+
+
+def fcg_cache_reset(cache: Cache, seq: int) -> None:
+    _check(_L.fcg_cache_reset(cache.h, int(seq)))
+
+
+def fcg_cache_export_layout(cache: Cache, seq: int, layer: int):
+    """-> (page_table int32 [n_lp] or None, seq_len, written uint8 [max_tokens])."""
+    pt = np.zeros(max(cache.n_lp, 1), dtype=np.int32)
+    n = C.c_int32()
+    wr = np.zeros(cache.max_tokens, dtype=np.uint8)
+    _check(_L.fcg_cache_export_layout(cache.h, int(seq), int(layer), _p(pt) if cache.page_size else None,
+                                      C.byref(n), wr.ctypes.data_as(C.POINTER(C.c_uint8))))
+    return (pt[:cache.n_lp] if cache.page_size else None), n.value, wr
+
+
+def fcg_cache_device_ptrs(cache: Cache, layer: int):
+    k, v = C.c_void_p(), C.c_void_p()
+    _check(_L.fcg_cache_device_ptrs(cache.h, int(layer), C.byref(k), C.byref(v)))
+    return k.value, v.value
+
+
+def fcg_cache_destroy(cache: Cache) -> None:
+    cache.close()
+
+
+def fcg_graft(cache: Cache, lib: Library, seq: Sequence[int], seg: Sequence[int], dst: Sequence[int],
+              stream=None) -> None:
+    s, g, d = _i32(seq), _i32(seg), _i32(dst)
+    if not (s.size == g.size == d.size):
+        raise ValueError("seq, seg and dst differ in length")
+    _check(_L.fcg_graft(cache.h, lib.h, int(s.size), _p(s), _p(g), _p(d), _stream(stream)))
+
+
+def fcg_patch_prefill(cache: Cache, layer: int, seq, pos, q, k, v, out, stream=None) -> None:
+    s, p = _i32(seq), _i32(pos)
+    if s.size != p.size:
+        raise ValueError("seq and pos differ in length")
+    _check(_L.fcg_patch_prefill(cache.h, int(layer), int(s.size), _p(s), _p(p), _dptr(q), _dptr(k), _dptr(v),
+                                _dptr(out), _stream(stream) if q is not None else None))
+
+
+def fcg_decode(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.ndarray:
+    s = _i32(seqs)
+    pos = np.zeros(max(s.size, 1), dtype=np.int32)
+    _check(_L.fcg_decode(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
+                         pos.ctypes.data_as(C.POINTER(C.c_int32)), _stream(stream) if q is not None else None))
+    return pos[:s.size]
+
+
+def fcg_status_string(status: int) -> str:
+    return _L.fcg_status_string(int(status)).decode()
+
+
+def fcg_last_error() -> str:
+    return _L.fcg_last_error().decode()

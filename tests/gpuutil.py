@@ -1,0 +1,129 @@
+"""Helpers of the GPU tests: device reads, oracle references, tolerance checks."""
+from __future__ import annotations
+
+import ctypes
+import sys
+
+import numpy as np
+import torch
+
+from oracle import graft as ograft, numerics, rope, task
+from paper_2606_13097_amd import fcg, synth
+
+_hip = None
+
+
+def _rt():
+    global _hip
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so.7")   # the runtime PyTorch already loaded
+        _hip.hipMemcpy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int]
+        _hip.hipMemcpy.restype = ctypes.c_int
+    return _hip
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def d2h(ptr: int, nbytes: int) -> np.ndarray:
+    torch.cuda.synchronize()
+    out = np.empty(nbytes, dtype=np.uint8)
+    rc = _rt().hipMemcpy(out.ctypes.data, ptr, nbytes, 2)
+    assert rc == 0, f"hipMemcpy failed: {rc}"
+    return out
+
+
+def storage_np(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().contiguous().cpu()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()
+
+
+def to_device(a: np.ndarray, dtype: str) -> torch.Tensor:
+    if dtype == "bf16":
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).cuda()
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def read_cache(cache: fcg.Cache, w: synth.Workload, layer: int, seq: int, positions) -> tuple:
+    """K, V of (layer, seq) at ``positions`` as storage arrays [n][Hkv][D]."""
+    sh = w.shape
+    H, D, es = sh.n_kv_heads, sh.head_dim, sh.elem_bytes
+    npdt = np.float32 if sh.dtype == "f32" else np.uint16
+    kp, vp = fcg.fcg_cache_device_ptrs(cache, layer)
+    positions = np.asarray(positions)
+    res = []
+    for base in (kp, vp):
+        if cache.page_size == 0:
+            off = seq * H * cache.max_tokens * D * es
+            raw = d2h(base + off, H * cache.max_tokens * D * es).view(npdt).reshape(H, cache.max_tokens, D)
+            res.append(np.ascontiguousarray(raw[:, positions].transpose(1, 0, 2)))
+        else:
+            pt, _, _ = fcg.fcg_cache_export_layout(cache, seq, layer)
+            P = cache.page_size
+            pool = d2h(base, cache.n_pages * H * P * D * es).view(npdt).reshape(cache.n_pages, H, P, D)
+            pages = pt[positions // P]
+            assert (pages >= 0).all()
+            res.append(np.ascontiguousarray(pool[pages, :, positions % P]))
+    return res[0], res[1]
+
+
+def oracle_items(w: synth.Workload, seq: int, layer: int):
+    m = w.graft_seq == seq
+    return [(int(d), int(w.lib_src_pos0[g]), synth.lib_segment(w, int(g), layer, "k"),
+             synth.lib_segment(w, int(g), layer, "v")) for g, d in zip(w.graft_seg[m], w.graft_dst[m])]
+
+
+def oracle_run(w: synth.Workload, seq: int, layer: int, n_decode: int, q_mult: float = 1.0):
+    """Oracle graft -> prefill -> decode for one sequence and layer, inputs from the host generator."""
+    sh = w.shape
+    pos, rows = w.fresh_of_seq(seq)
+    fq = synth.fresh_tokens(w, seq, layer, "q", rows)
+    if q_mult != 1.0:
+        fq = scale_storage(fq, q_mult, sh.dtype)
+    fk = synth.fresh_tokens(w, seq, layer, "k", rows)
+    fv = synth.fresh_tokens(w, seq, layer, "v", rows)
+    steps = np.arange(n_decode)
+    dq = synth.decode_tokens(w, seq, layer, "q", steps) if n_decode else []
+    dk = synth.decode_tokens(w, seq, layer, "k", steps) if n_decode else []
+    dv = synth.decode_tokens(w, seq, layer, "v", steps) if n_decode else []
+    return task.run_layer(sh.n_q_heads, sh.n_kv_heads, sh.head_dim, sh.rope_theta, sh.dtype, w.max_tokens,
+                          oracle_items(w, seq, layer), pos, fq, fk, fv, list(dq), list(dk), list(dv))
+
+
+def scale_storage(x: np.ndarray, mult: float, dtype: str) -> np.ndarray:
+    """Multiply storage values by a power of two (exact)."""
+    return numerics.encode(numerics.decode(x, dtype) * mult, dtype)
+
+
+def check_attn(got_storage: np.ndarray, ref: np.ndarray, dtype: str, what: str) -> None:
+    """fp32: normwise 1e-5 per head; bf16: max-abs 2e-2 and relative Frobenius 1e-2."""
+    got = numerics.decode(got_storage, dtype)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.isfinite(got).all(), f"{what}: non-finite output"
+    if dtype == "f32":
+        for h in range(ref.shape[-2]):
+            den = np.abs(ref[..., h, :]).max()
+            err = np.abs(got[..., h, :] - ref[..., h, :]).max()
+            assert err <= 1e-5 * den, f"{what}: head {h} normwise error {err / den:.3e} > 1e-5"
+    else:
+        err = np.abs(got - ref).max()
+        fro = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+        assert err <= 2e-2, f"{what}: max-abs error {err:.3e} > 2e-2"
+        assert fro <= 1e-2, f"{what}: relative Frobenius error {fro:.3e} > 1e-2"
+
+
+def check_keys(got_storage: np.ndarray, ref_rounded: np.ndarray, dtype: str, what: str) -> None:
+    """Grafted / appended keys: fp32 normwise 1e-5; bf16 within one unit in the last place."""
+    got = numerics.decode(got_storage, dtype)
+    if dtype == "f32":
+        den = np.abs(ref_rounded).max()
+        err = np.abs(got - ref_rounded).max()
+        assert err <= 1e-5 * den, f"{what}: normwise error {err / den:.3e}"
+    else:
+        step = numerics.ulp(ref_rounded, dtype)
+        bad = np.abs(got - ref_rounded) > step
+        assert not bad.any(), f"{what}: {int(bad.sum())} keys off by more than 1 ulp"

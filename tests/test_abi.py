@@ -1,0 +1,45 @@
+"""The C-ABI library loads on the CPU and exports every symbol include/fcg.h declares."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fcg.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:fcg_status|const char\*)\s+(fcg_\w+)\s*\(", text, re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    for n in ("fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_lib_create", "fcg_cache_create"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2606_13097_amd import fcg
+    lib = ctypes.CDLL(fcg.LIB_PATH)
+    missing = [n for n in _declared() if not hasattr(lib, n)]
+    assert not missing
+    assert sorted(fcg.EXPORTS) == _declared()
+
+
+def test_status_strings_and_errors_without_gpu():
+    from paper_2606_13097_amd import fcg
+    for i, name in enumerate(fcg.STATUS):
+        assert fcg.fcg_status_string(i) == name
+    bad = fcg.model_desc(1, 4, 3, 64, 1e4, "f32")            # 4 % 3 != 0
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.Cache(bad, 1, 16, flags=fcg.FCG_LAYOUT_ONLY)
+    assert e.value.status == fcg.FCG_EINVAL and "multiple" in fcg.fcg_last_error()
+    for hd in (32, 96, 256):
+        with pytest.raises(fcg.FcgError):
+            fcg.Cache(fcg.model_desc(1, 4, 2, hd, 1e4, "bf16"), 1, 16, flags=fcg.FCG_LAYOUT_ONLY)
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.Cache(fcg.model_desc(1, 4, 2, 64, 1e4, "bf16"), 1, 16, page_size=8, n_pages=4,
+                  flags=fcg.FCG_LAYOUT_ONLY)
+    assert e.value.status == fcg.FCG_EINVAL

@@ -1,0 +1,286 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, on seeded synthetic workloads.
+
+Bars: layout and placement bit-exact; grafted and copied values bit-exact; grafted keys
+within 1e-5 normwise (fp32) or one bf16 ulp; attention outputs within 1e-5 normwise per
+head (fp32) or max-abs 2e-2 plus relative Frobenius 1e-2 (bf16).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpuutil import (check_attn, check_keys, oracle_items, oracle_run, read_cache, say, storage_np, to_device)
+from oracle import graft as ograft, numerics, rope
+from oracle.layout import Layout
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    from paper_2606_13097_amd import fcg, runner, synth  # noqa: F401  (fails loudly if unbuilt)
+    yield
+
+
+def _oracle_layout(w, n_decode, layers):
+    ora = Layout(w.shape.n_layers, w.n_seqs, w.max_tokens, w.page_size, w.n_pages, w.lib_lengths, w.lib_src_pos0)
+    ora.graft(w.graft_seq, w.graft_seg, w.graft_dst)
+    for layer in layers:
+        ora.append(layer, w.fresh_seq, w.fresh_pos)
+        for _ in range(n_decode):
+            ora.decode(layer, list(range(w.n_seqs)))
+    return ora
+
+
+def _compare_layout(cache, ora, w, layers):
+    from paper_2606_13097_amd import fcg
+    for s in range(w.n_seqs):
+        for layer in layers:
+            pt, n, wr = fcg.fcg_cache_export_layout(cache, s, layer)
+            np.testing.assert_array_equal(wr.astype(bool), ora.written[s, layer])
+            assert n == ora.seq_len(s, layer)
+            if w.page_size:
+                np.testing.assert_array_equal(pt, ora.page_table[s])
+
+
+def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False):
+    from paper_2606_13097_amd import runner
+    sh = w.shape
+    say(f"[gpu] pipeline {w.name} L={sh.n_layers} seqs={w.n_seqs} decode={n_decode} q_mult={q_mult} "
+        f"shuffle={shuffle} page={w.page_size}")
+    setup = runner.GpuSetup(w)
+    try:
+        setup.graft()
+        torch.cuda.synchronize()
+        say("[gpu]   graft done")
+        w_items = {}
+        for layer in layers:
+            w_inv = rope.inv_freq(sh.head_dim, sh.rope_theta)
+            for s in check_seqs:
+                items = oracle_items(w, s, layer)
+                w_items[(s, layer)] = items
+                K, V, wr = ograft.compose(w.max_tokens, sh.n_kv_heads, sh.head_dim, items, w_inv, sh.dtype)
+                pos = np.flatnonzero(wr)
+                gk, gv = read_cache(setup.cache, w, layer, s, pos)
+                np.testing.assert_array_equal(numerics.decode(gv, sh.dtype), V[pos])
+                check_keys(gk, K[pos], sh.dtype, f"graft keys seq {s} layer {layer}")
+                # segments whose delta is 0 are copied bit for bit
+                for dst, src, k_lib, _ in items:
+                    if dst == src:
+                        gk0, _ = read_cache(setup.cache, w, layer, s, np.arange(dst, dst + k_lib.shape[0]))
+                        np.testing.assert_array_equal(gk0, k_lib)
+        outs = {}
+        order = np.arange(len(w.fresh_pos))
+        if shuffle:
+            order = np.random.default_rng(0).permutation(order)
+        for layer in layers:
+            q, k, v = setup.fresh_inputs(layer)
+            if q_mult != 1.0:
+                q = q * q_mult
+            q, k, v = q[order].contiguous(), k[order].contiguous(), v[order].contiguous()
+            out = torch.empty_like(q)
+            from paper_2606_13097_amd import fcg
+            fcg.fcg_patch_prefill(setup.cache, layer, w.fresh_seq[order], w.fresh_pos[order], q, k, v, out)
+            res = torch.empty_like(out)
+            res[torch.from_numpy(order).cuda()] = out
+            outs[("prefill", layer)] = res
+        torch.cuda.synchronize()
+        say("[gpu]   prefill done")
+        for layer in layers:
+            dq, dk, dv = setup.decode_inputs(layer, n_decode)
+            if q_mult != 1.0:
+                dq = dq * q_mult
+            douts = []
+            for t in range(n_decode):
+                o = torch.empty_like(dq[t])
+                setup.decode(layer, dq[t], dk[t], dv[t], o)
+                douts.append(o)
+            outs[("decode", layer)] = douts
+        torch.cuda.synchronize()
+        say("[gpu]   decode done")
+        ora = _oracle_layout(w, n_decode, layers)
+        _compare_layout(setup.cache, ora, w, layers)
+        for layer in layers:
+            for s in check_seqs:
+                ref = oracle_run(w, s, layer, n_decode, q_mult)
+                idx = np.flatnonzero(w.fresh_seq == s)
+                got = storage_np(outs[("prefill", layer)][idx])
+                check_attn(got, ref["prefill"], sh.dtype, f"prefill seq {s} layer {layer}")
+                for t in range(n_decode):
+                    got = storage_np(outs[("decode", layer)][t][s])
+                    check_attn(got, ref["decode"][t], sh.dtype, f"decode seq {s} layer {layer} step {t}")
+                # final cache: fresh and decode keys/values placed at their positions
+                pos = np.flatnonzero(ref["written"])
+                gk, gv = read_cache(setup.cache, w, layer, s, pos)
+                np.testing.assert_array_equal(numerics.decode(gv, sh.dtype), ref["V"][pos])
+                check_keys(gk, ref["K"][pos], sh.dtype, f"final keys seq {s} layer {layer}")
+        say("[gpu]   parity ok")
+    finally:
+        setup.close()
+
+
+def test_tiny_fp32_pipeline():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("tiny", seed=1)
+    run_pipeline(w, [0], 8, [0])
+
+
+def test_tiny_fp32_shuffled_tokens_and_seed():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("tiny", seed=3)
+    run_pipeline(w, [0], 3, [0], shuffle=True)
+
+
+def test_7b_shape_bf16_two_layers():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("7b", seed=1, n_layers=2, n_lib=24)
+    run_pipeline(w, [0, 1], 5, [0])
+
+
+def test_7b_shape_bf16_peaked_queries():
+    """Q x 8 gives score std ~4: attention far from uniform, so a tolerance of 2e-2 is not vacuous."""
+    from paper_2606_13097_amd import synth
+    w = synth.workload("7b", seed=2, n_layers=1, n_lib=16)
+    run_pipeline(w, [0], 3, [0], q_mult=8.0)
+
+
+def test_negative_and_positive_deltas_bf16():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("7b", seed=4, n_layers=1, n_lib=16)
+    rng = np.random.default_rng(4)
+    w.lib_src_pos0 = rng.integers(0, 9000, size=len(w.lib_lengths)).astype(np.int32)
+    run_pipeline(w, [0], 2, [0], shuffle=True)
+
+
+def test_long_context_gap_tokens_bf16():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("long16k", seed=1, n_layers=1, n_lib=24)
+    run_pipeline(w, [0], 2, [0])
+
+
+def test_batched_paged_bf16():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("batched", seed=1, n_layers=1, n_lib=48)
+    run_pipeline(w, [0], 3, [0, 7, 31])
+
+
+def test_34b_shape_outliers_bf16():
+    from paper_2606_13097_amd import synth
+    w = synth.workload("34b", seed=1, n_layers=1, n_lib=40)
+    # keep the oracle quick: 6 segments and 64 patch tokens per task
+    keep = np.zeros(len(w.graft_seq), bool)
+    for t in range(w.n_seqs):
+        keep[np.flatnonzero(w.graft_seq == t)[:6]] = True
+    w.graft_seq, w.graft_seg, w.graft_dst = w.graft_seq[keep], w.graft_seg[keep], w.graft_dst[keep]
+    fresh = []
+    for t in range(w.n_seqs):
+        end = int((w.graft_dst[w.graft_seq == t] + w.lib_lengths[w.graft_seg[w.graft_seq == t]]).max())
+        fresh += [(t, end + j, j) for j in range(64)]
+    w.fresh_seq = np.array([f[0] for f in fresh], np.int32)
+    w.fresh_pos = np.array([f[1] for f in fresh], np.int32)
+    w.fresh_row = np.array([f[2] for f in fresh], np.int32)
+    run_pipeline(w, [0], 2, [0, 3])
+
+
+def test_causality_future_positions_do_not_change_outputs():
+    """A segment grafted beyond every query position leaves prefill outputs bit-identical."""
+    from paper_2606_13097_amd import fcg, runner, synth
+    w = synth.workload("7b", seed=5, n_layers=1, n_lib=16)
+    w.max_tokens += 2048
+    say("[gpu] causality")
+    a = runner.GpuSetup(w, n_caches=2)
+    try:
+        a.graft(a.caches[0])
+        a.graft(a.caches[1])
+        top = int(w.fresh_pos.max()) + 1
+        fcg.fcg_graft(a.caches[1], a.lib, [0], [0], [top + 5])
+        q, k, v = a.fresh_inputs(0)
+        o1, o2 = torch.empty_like(q), torch.empty_like(q)
+        a.prefill(0, q, k, v, o1, cache=a.caches[0])
+        a.prefill(0, q, k, v, o2, cache=a.caches[1])
+        torch.cuda.synchronize()
+        assert torch.equal(o1.view(torch.int16), o2.view(torch.int16))
+    finally:
+        a.close()
+
+
+def test_needle_through_gpu_graft():
+    """Keys encoded at 0..63, grafted at 3000: a query aimed at one of them retrieves its value."""
+    from paper_2606_13097_amd import fcg
+    D, Hkv, Hq, theta, dt = 128, 2, 8, 1e6, "bf16"
+    say("[gpu] needle")
+    desc = fcg.model_desc(1, Hq, Hkv, D, theta, dt)
+    rng = np.random.default_rng(12)
+    w = rope.inv_freq(D, theta)
+    n = 64
+    k_raw = rng.standard_normal((n, Hkv, D)) * 0.5
+    j = 23
+    k_raw[j] *= 2.0
+    k_raw[j, :, 16:64] = 0.0
+    k_raw[j, :, 80:] = 0.0
+    k_lib = numerics.encode(rope.rotate(k_raw, np.arange(n)[:, None], w), dt)
+    v_lib = np.zeros((n, Hkv, D))
+    v_lib[j] = 1.0
+    v_lib = numerics.encode(v_lib, dt)
+    filler_k = numerics.encode(rng.standard_normal((3000, Hkv, D)) * 0.5, dt)
+    filler_v = numerics.encode(np.zeros((3000, Hkv, D)), dt)
+    lib = fcg.Library(desc, 3064, 2)
+    fcg.fcg_lib_add_segment(lib, 3000, 0, to_device(filler_k, dt), to_device(filler_v, dt))
+    fcg.fcg_lib_add_segment(lib, n, 0, to_device(k_lib, dt), to_device(v_lib, dt))
+    cache = fcg.Cache(desc, 1, 4096)
+    fcg.fcg_graft(cache, lib, [0, 0], [0, 1], [0, 3000])
+    p_q = 3064
+    p_k = 3000 + j
+    q_raw = np.zeros((1, Hq, D))
+    for hq in range(Hq):
+        q_raw[0, hq] = 8.0 * rope.rotate(k_raw[j, hq // (Hq // Hkv)], p_k - p_q, w)
+    q = to_device(numerics.encode(q_raw, dt), dt)
+    kk = to_device(numerics.encode(np.zeros((1, Hkv, D)), dt), dt)
+    out = torch.empty_like(q)
+    fcg.fcg_patch_prefill(cache, 0, [0], [p_q], q, kk, kk, out)
+    o = numerics.decode(storage_np(out), dt)
+    assert np.all(o > 0.98), o.min()
+    cache.close()
+    lib.close()
+
+
+def test_errors_on_device_cache_change_nothing():
+    from paper_2606_13097_amd import fcg, runner, synth
+    w = synth.workload("tiny", seed=1)
+    say("[gpu] errors")
+    s = runner.GpuSetup(w)
+    try:
+        s.graft()
+        before = fcg.fcg_cache_export_layout(s.cache, 0, 0)
+        with pytest.raises(fcg.FcgError) as e:
+            s.graft()
+        assert e.value.status == fcg.FCG_EOVERLAP
+        q, k, v = s.fresh_inputs(0)
+        out = torch.empty_like(q)
+        with pytest.raises(fcg.FcgError) as e:
+            fcg.fcg_patch_prefill(s.cache, 0, [0], [int(w.fresh_pos.max()) + 3], q[:1], k[:1], v[:1], out[:1])
+        assert e.value.status == fcg.FCG_EHOLE
+        with pytest.raises(fcg.FcgError) as e:
+            fcg.fcg_decode(s.cache, 1, [0], q[:1], k[:1], v[:1], out[:1])
+        assert e.value.status == fcg.FCG_ERANGE
+        after = fcg.fcg_cache_export_layout(s.cache, 0, 0)
+        assert after[1] == before[1] and np.array_equal(after[2], before[2])
+        # empty calls are no-ops
+        fcg.fcg_graft(s.cache, s.lib, [], [], [])
+        fcg.fcg_patch_prefill(s.cache, 0, [], [], q, k, v, out)
+        assert len(fcg.fcg_decode(s.cache, 0, [], q, k, v, out)) == 0
+        torch.cuda.synchronize()
+    finally:
+        s.close()
+
+
+def test_synth_gpu_twin_matches_host_bits():
+    from paper_2606_13097_amd import synth
+    from paper_2606_13097_amd.synth import gpu as sg
+    say("[gpu] synth twin")
+    for dt, rate in (("f32", 0.0), ("bf16", 0.0), ("bf16", 0.05)):
+        t = torch.empty((37, 8, 128), dtype=torch.float32 if dt == "f32" else torch.bfloat16, device="cuda")
+        sg.fill_rows(t, dt, 7, "lib_k", 3, 11, 5, 0.5, rate)
+        ref = synth.tensor_values(7, "lib_k", 3, 11, np.arange(5, 42), 8, 128, 0.5, dt, rate)
+        np.testing.assert_array_equal(storage_np(t), ref)
