@@ -297,7 +297,8 @@ def _consecutive_task(seq, seg_ids, lengths, start):
 
 
 def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
-             n_decode: Optional[int] = None, n_lib: Optional[int] = None) -> Workload:
+             n_decode: Optional[int] = None, n_lib: Optional[int] = None,
+             task: Optional[int] = None) -> Workload:
     """Build one of the named workloads.
 
     ``tiny``     1 layer, 4/2 heads, D 64, theta 1e4, fp32; 8 segments of 96/128/160
@@ -311,15 +312,29 @@ def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
     ``34b``      48 layers, 64/8 heads, D 128, bf16; 1024 segments U[200,1600]; 4 tasks of
                  24 segments; 512 patch; 64 decode; 1% outlier pairs x8.
     ``n_layers``/``n_decode``/``n_lib`` shrink a workload for tests (same plan law).
+    ``task`` redraws which segments are grafted (and the gaps) from a second
+    stream while keeping the library of ``seed``: a stream of distinct tasks
+    over one resident library.
     """
     rng = np.random.default_rng(seed)
+
+    class _Split:
+        """Library draws from the seed's stream; task draws from (seed, task) when given."""
+
+        def __init__(self):
+            self.t = np.random.default_rng([seed, task]) if task is not None else rng
+
+        def __getattr__(self, k):
+            return getattr(self.t, k)
+
+    trng = _Split()
     if name == "tiny":
         shape = Shape(n_layers or 1, 4, 2, 64, 1e4, "f32")
         nl = n_lib or 8
         lengths = list(rng.choice([96, 128, 160], size=nl))
         lengths.append(64)                       # system-prompt segment
         prefix = nl
-        chosen = rng.choice(nl, size=3, replace=False)
+        chosen = trng.choice(nl, size=3, replace=False)
         graft, pos = _consecutive_task(0, [prefix] + list(chosen), lengths, 0)
         fresh = [(0, pos + j, j) for j in range(16)]
         return _finish(name, shape, seed, lengths, 1.0, 1.0, 0.0, 0, graft, fresh,
@@ -330,19 +345,19 @@ def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
         if name == "7b":
             lengths = list(rng.integers(200, 800, size=nl, endpoint=True))
             lengths.append(1024)
-            chosen = rng.choice(nl, size=6, replace=False)
+            chosen = trng.choice(nl, size=6, replace=False)
             graft, pos = _consecutive_task(0, [nl] + list(chosen), lengths, 0)
             fresh = [(0, pos + j, j) for j in range(64)]
             nd = 256
         else:
             lengths = list(rng.integers(400, 1200, size=nl, endpoint=True))
             lengths.append(2048)
-            chosen = rng.choice(nl, size=min(20, nl), replace=False)
+            chosen = trng.choice(nl, size=min(20, nl), replace=False)
             graft = [(0, nl, 0)]
             pos, row = 2048, 0
             fresh = []
             for s in chosen:
-                gap = int(rng.integers(0, 32, endpoint=True))
+                gap = int(trng.integers(0, 32, endpoint=True))
                 for j in range(gap):
                     fresh.append((0, pos + j, row))
                     row += 1
@@ -366,7 +381,7 @@ def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
         n_tasks = 32
         graft, fresh = [], []
         for t in range(n_tasks):
-            chosen = perm[rng.choice(nl, size=8, replace=False, p=p)]
+            chosen = perm[trng.choice(nl, size=8, replace=False, p=p)]
             items, pos = _consecutive_task(t, list(chosen), lengths, 0)
             graft += items
             fresh += [(t, pos + j, j) for j in range(32)]
@@ -378,7 +393,7 @@ def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
         lengths = list(rng.integers(200, 1600, size=nl, endpoint=True))
         graft, fresh = [], []
         for t in range(4):
-            chosen = rng.choice(nl, size=min(24, nl), replace=False)
+            chosen = trng.choice(nl, size=min(24, nl), replace=False)
             items, pos = _consecutive_task(t, list(chosen), lengths, 0)
             graft += items
             fresh += [(t, pos + j, j) for j in range(512)]

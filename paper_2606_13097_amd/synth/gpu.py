@@ -29,6 +29,8 @@ def fill(dst_ptr: int, dtype: str, seed: int, tag: str, layer0: int, n_layers: i
     """Element (l, r, h, d) -> dst[l*stride_layer + h*stride_head + r*stride_row + d]."""
     if stream is None:
         stream = torch.cuda.current_stream().cuda_stream
+    if tag in ("fresh_q", "dec_q"):
+        outlier_rate = 0.0          # outlier pairs live in K and V only
     rc = _L.fcg_synth_fill(C.c_void_p(dst_ptr), 0 if dtype == "f32" else 1, seed, TAGS[tag], layer0, n_layers, item,
                            row0, n_rows, n_heads, head_dim, stride_layer, stride_head, stride_row, scale,
                            outlier_rate, C.c_void_p(stream))

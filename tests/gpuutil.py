@@ -88,6 +88,8 @@ def oracle_run(w: synth.Workload, seq: int, layer: int, n_decode: int, q_mult: f
     fv = synth.fresh_tokens(w, seq, layer, "v", rows)
     steps = np.arange(n_decode)
     dq = synth.decode_tokens(w, seq, layer, "q", steps) if n_decode else []
+    if n_decode and q_mult != 1.0:
+        dq = scale_storage(dq, q_mult, sh.dtype)
     dk = synth.decode_tokens(w, seq, layer, "k", steps) if n_decode else []
     dv = synth.decode_tokens(w, seq, layer, "v", steps) if n_decode else []
     return task.run_layer(sh.n_q_heads, sh.n_kv_heads, sh.head_dim, sh.rope_theta, sh.dtype, w.max_tokens,
@@ -100,7 +102,12 @@ def scale_storage(x: np.ndarray, mult: float, dtype: str) -> np.ndarray:
 
 
 def check_attn(got_storage: np.ndarray, ref: np.ndarray, dtype: str, what: str) -> None:
-    """fp32: normwise 1e-5 per head; bf16: max-abs 2e-2 and relative Frobenius 1e-2."""
+    """fp32: normwise 1e-5 per head; bf16: max-abs 2e-2 * max(1, max|ref|) and relative Frobenius 1e-2.
+
+    The 2e-2 max-abs bar is for unit-scale outputs: bf16 storage of an output of size |o|
+    alone carries up to 2^-9 |o| of rounding, so workloads whose values reach |o| > 1 (the
+    x8 outlier channels) scale the bar with the largest reference magnitude.
+    """
     got = numerics.decode(got_storage, dtype)
     assert got.shape == ref.shape, (got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{what}: non-finite output"
@@ -112,18 +119,32 @@ def check_attn(got_storage: np.ndarray, ref: np.ndarray, dtype: str, what: str) 
     else:
         err = np.abs(got - ref).max()
         fro = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
-        assert err <= 2e-2, f"{what}: max-abs error {err:.3e} > 2e-2"
+        lim = 2e-2 * max(1.0, float(np.abs(ref).max()))
+        assert err <= lim, f"{what}: max-abs error {err:.3e} > {lim:.3e}"
         assert fro <= 1e-2, f"{what}: relative Frobenius error {fro:.3e} > 1e-2"
 
 
 def check_keys(got_storage: np.ndarray, ref_rounded: np.ndarray, dtype: str, what: str) -> None:
-    """Grafted / appended keys: fp32 normwise 1e-5; bf16 within one unit in the last place."""
+    """Grafted / appended keys.
+
+    fp32: normwise 1e-5.  bf16: |got - ref| <= ulp(ref) + 2^-20 * |pair|, per element.  The
+    kernel turns a pair (x_i, x_{i+D/2}) in fp32 with fp32 cos/sin: its result is within
+    about 2^-22 (|x_i| + |x_{i+D/2}|) of the exact value (cos/sin, product and fma roundings),
+    and the pair norm is kept by the turn; rounding that to bf16 can land one bf16 step away
+    from the rounding of the exact value.  A component much smaller than its pair can
+    therefore differ by more than one of its own ulps; the pair-norm term covers that.
+    """
     got = numerics.decode(got_storage, dtype)
     if dtype == "f32":
         den = np.abs(ref_rounded).max()
         err = np.abs(got - ref_rounded).max()
         assert err <= 1e-5 * den, f"{what}: normwise error {err / den:.3e}"
     else:
-        step = numerics.ulp(ref_rounded, dtype)
-        bad = np.abs(got - ref_rounded) > step
-        assert not bad.any(), f"{what}: {int(bad.sum())} keys off by more than 1 ulp"
+        half = ref_rounded.shape[-1] // 2
+        pair = np.hypot(ref_rounded[..., :half], ref_rounded[..., half:])
+        pair = np.concatenate([pair, pair], axis=-1)
+        tol = numerics.ulp(ref_rounded, dtype) + 2.0 ** -20 * pair
+        bad = np.abs(got - ref_rounded) > tol
+        assert not bad.any(), f"{what}: {int(bad.sum())} keys outside one ulp + 2^-20 |pair|"
+        n_off = int((got != ref_rounded).sum())
+        assert n_off <= 0.01 * got.size, f"{what}: {n_off} of {got.size} keys differ from the oracle's rounding"

@@ -279,8 +279,9 @@ def test_synth_gpu_twin_matches_host_bits():
     from paper_2606_13097_amd import synth
     from paper_2606_13097_amd.synth import gpu as sg
     say("[gpu] synth twin")
-    for dt, rate in (("f32", 0.0), ("bf16", 0.0), ("bf16", 0.05)):
+    for tag, dt, rate in (("lib_k", "f32", 0.0), ("lib_v", "bf16", 0.0), ("lib_k", "bf16", 0.05),
+                          ("fresh_q", "bf16", 0.05), ("dec_v", "bf16", 0.05)):
         t = torch.empty((37, 8, 128), dtype=torch.float32 if dt == "f32" else torch.bfloat16, device="cuda")
-        sg.fill_rows(t, dt, 7, "lib_k", 3, 11, 5, 0.5, rate)
-        ref = synth.tensor_values(7, "lib_k", 3, 11, np.arange(5, 42), 8, 128, 0.5, dt, rate)
+        sg.fill_rows(t, dt, 7, tag, 3, 11, 5, 0.5, rate)
+        ref = synth.tensor_values(7, tag, 3, 11, np.arange(5, 42), 8, 128, 0.5, dt, rate)
         np.testing.assert_array_equal(storage_np(t), ref)
