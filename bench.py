@@ -1,0 +1,280 @@
+#!/usr/bin/env python3
+"""Benchmark of the function-level KV grafting hot path on one MI355X.
+
+One step = one task of the 7B-class workload (32 layers, 32 query / 8 kv heads,
+head_dim 128, bf16, ~4K grafted tokens): cache-stitching of the system prompt
+and 6 retrieved segments (fcg_graft, one launch for all layers), patch prefill
+of 64 tokens (fcg_patch_prefill, one call per layer) and 256 decode steps
+(fcg_decode, one call per layer and step).  Every step grafts a different
+seeded task over the same resident 17 GB segment library, so grafted bytes
+come from HBM, not from the last-level cache.
+
+Prints ONE JSON line.  ``value`` is the graft throughput in GB/s (algorithmic
+bytes: every grafted K and V element read once and written once, divided by
+the measured graft time); the patch-attention TFLOP/s and the decode GB/s are
+reported beside it, each with its roofline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "graft GB/s + patch-attn TFLOP/s (frac of MI355X peak), 7B GQA, 4K grafted ctx"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--workload", default="7b")
+    ap.add_argument("--seed", type=int, default=1)
+    ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-gib", type=float, default=0.0,
+                    help="only run a plain device copy of this size (HBM counter calibration)")
+    return ap.parse_args()
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def measured_traffic(name):
+    """HBM bytes per launch from a committed counter summary, if the kernel source is unchanged."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    from paper_2606_13097_amd.profiling import source_sha256
+    with open(path) as f:
+        d = json.load(f)
+    if d.get("source_sha256") != source_sha256(d["source"]):
+        return None
+    return int(round(d["traffic_bytes_per_launch"]))
+
+
+def copy_probe(gib: float) -> None:
+    import torch
+    n = int(gib * (1 << 30)) // 2
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    log(f"copy probe: {n * 2} bytes read, {n * 2} bytes written")
+
+
+def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    import numpy as np
+    from oracle import attention as oatt, graft as ograft, numerics, rope
+    from paper_2606_13097_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        blas_threads = os.cpu_count() or 1
+    sh = w.shape
+    tw = task_ws[0]
+    winv = rope.inv_freq(sh.head_dim, sh.rope_theta)
+    # graft sample: every grafted segment of one task at n_layers_graft layers
+    inputs = []
+    for layer in range(n_layers_graft):
+        for g, d in zip(tw.graft_seg, tw.graft_dst):
+            inputs.append((int(d) - int(tw.lib_src_pos0[g]), synth.lib_segment(tw, int(g), layer, "k"),
+                           synth.lib_segment(tw, int(g), layer, "v")))
+    # repeat the sample until about 10 s of CPU work have been timed
+    reps, t_graft = 0, 0.0
+    while t_graft < 10.0 and reps < 64:
+        t0 = time.perf_counter()
+        for delta, k, v in inputs:
+            kk = ograft.graft_keys(k, delta, winv, sh.dtype)
+            vv = ograft.graft_values(v, sh.dtype)
+            numerics.encode(kk, sh.dtype), numerics.encode(vv, sh.dtype)
+        t_graft += time.perf_counter() - t0
+        reps += 1
+    graft_bytes = 2 * tw.grafted_tokens * 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes * n_layers_graft * reps
+    # patch-attention sample: the 64 patch tokens at n_layers_attn layers
+    flops = 0
+    t_att = 0.0
+    for layer in range(n_layers_attn):
+        items = [(int(d), int(tw.lib_src_pos0[g]), synth.lib_segment(tw, int(g), layer, "k"),
+                  synth.lib_segment(tw, int(g), layer, "v")) for g, d in zip(tw.graft_seg, tw.graft_dst)]
+        K, V, wr = ograft.compose(tw.max_tokens, sh.n_kv_heads, sh.head_dim, items, winv, sh.dtype)
+        pos, rows = tw.fresh_of_seq(0)
+        fq = synth.fresh_tokens(tw, 0, layer, "q", rows)
+        fk = synth.fresh_tokens(tw, 0, layer, "k", rows)
+        fv = synth.fresh_tokens(tw, 0, layer, "v", rows)
+        ograft.place_fresh(K, V, wr, pos, fk, fv, winv, sh.dtype)
+        qe = ograft.encode_fresh(fq, pos, winv, sh.dtype)
+        t0 = time.perf_counter()
+        oatt.attend(qe, pos, K, V, wr)
+        t_att += time.perf_counter() - t0
+        flops += 4 * sh.n_q_heads * sh.head_dim * int((pos + 1).sum())
+    return {
+        "value": round(graft_bytes / t_graft / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+        "sample": f"graft of one task's {len(tw.graft_seg)} segments ({tw.grafted_tokens} tokens) at "
+                  f"{n_layers_graft} of {sh.n_layers} layers, {reps} passes: {graft_bytes / 1e6:.1f} MB in "
+                  f"{t_graft:.2f} s (NumPy float64, single thread)",
+        "patch_attn": {"value": round(flops / t_att / 1e12, 6), "unit": "TFLOP/s", "cores": blas_threads,
+                       "sample": f"64 patch tokens x {sh.n_q_heads} heads at {n_layers_attn} layers, "
+                                 f"{flops / 1e9:.2f} GFLOP in {t_att:.2f} s (NumPy float64 + BLAS)"},
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build runs the grafting path on a single MI355X "
+              f"with no sharding (asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    from paper_2606_13097_amd import fcg, runner, synth
+
+    if args.copy_probe_gib > 0:
+        copy_probe(args.copy_probe_gib)
+        return
+    torch.cuda.set_device(0)
+    nd = args.decode_steps
+    w = synth.workload(args.workload, seed=args.seed, n_decode=nd)
+    sh = w.shape
+    n_tasks = args.steps + args.warmup
+    task_ws = [synth.workload(args.workload, seed=args.seed, n_decode=nd, task=t) for t in range(n_tasks)]
+    w.max_tokens = max(t.max_tokens for t in task_ws)
+    log(f"bench: building the {w.name} segment library ({len(w.lib_lengths)} segments, "
+        f"{int(w.lib_lengths.sum()) * sh.token_bytes / 1e9:.1f} GB)")
+    t0 = time.time()
+    setup = runner.GpuSetup(w)
+    log(f"bench: library ready in {time.time() - t0:.1f} s")
+    fresh = [setup.fresh_inputs(l) for l in range(sh.n_layers)]
+    dec = [setup.decode_inputs(l) for l in range(sh.n_layers)]
+    outs_p = [torch.empty_like(f[0]) for f in fresh]
+    out_d = torch.empty_like(dec[0][0][0])
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    cache = setup.cache
+    lib = setup.lib
+    all_seqs = np.arange(w.n_seqs)
+
+    def ev():
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(stream)
+        return e
+
+    def run_task(tw):
+        for s in range(w.n_seqs):
+            fcg.fcg_cache_reset(cache, s)
+        e0 = ev()
+        fcg.fcg_graft(cache, lib, tw.graft_seq, tw.graft_seg, tw.graft_dst)
+        e1 = ev()
+        for l in range(sh.n_layers):
+            q, k, v = fresh[l]
+            fcg.fcg_patch_prefill(cache, l, tw.fresh_seq, tw.fresh_pos, q, k, v, outs_p[l])
+        e2 = ev()
+        for t in range(tw.n_decode):
+            for l in range(sh.n_layers):
+                dq, dk, dv = dec[l]
+                fcg.fcg_decode(cache, l, all_seqs, dq[t], dk[t], dv[t], out_d)
+        e3 = ev()
+        return e0, e1, e2, e3
+
+    for i in range(args.warmup):
+        run_task(task_ws[args.steps + i])
+    torch.cuda.synchronize()
+    for kind in range(4):
+        fcg.fcg_cache_timing_read(cache, kind)        # drop anything recorded so far
+    log(f"bench: warmup done; timing {args.steps} steps")
+    fcg.fcg_cache_timing(cache, True)                  # HIP events around the library's own kernels
+    marks = []
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        marks.append((task_ws[i], run_task(task_ws[i])))
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    fcg.fcg_cache_timing(cache, False)
+    log(f"bench: timed steps done in {t_wall:.2f} s")
+    kt = {k: fcg.fcg_cache_timing_read(cache, k) for k in range(4)}
+
+    g_bytes = g_ms = p_flops = p_ms = d_bytes = d_ms = 0.0
+    n_dec_calls = 0
+    kvb = 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes          # K+V bytes of one token in one layer
+    for tw, (e0, e1, e2, e3) in marks:
+        g_ms += e0.elapsed_time(e1)
+        p_ms += e1.elapsed_time(e2)
+        d_ms += e2.elapsed_time(e3)
+        g_bytes += 2 * tw.grafted_tokens * kvb * sh.n_layers
+        p_flops += 4 * sh.n_q_heads * sh.head_dim * float((tw.fresh_pos.astype(np.int64) + 1).sum()) * sh.n_layers
+        ctx = tw.seq_len_after_prefill(0)
+        d_bytes += sum((ctx + t + 1) * kvb for t in range(tw.n_decode)) * sh.n_layers
+        n_dec_calls += tw.n_decode * sh.n_layers
+    K = args.steps
+    (ng, g_kms), (na, a_kms), (npf, p_kms), (nd_, d_kms) = kt[0], kt[1], kt[2], kt[3]
+    assert ng == K and na == K * sh.n_layers and npf == K * sh.n_layers and nd_ == n_dec_calls, kt
+    graft_gbs = g_bytes / (g_kms / 1e3) / 1e9                  # graft kernel
+    attn_tflops = p_flops / (a_kms / 1e3) / 1e12               # MFMA attention kernel
+    prefill_tflops = p_flops / (p_kms / 1e3) / 1e12            # append + attention + merge kernels
+    decode_gbs = d_bytes / (d_kms / 1e3) / 1e9                 # decode + merge kernels
+    ms_per_step = (g_ms + p_ms + d_ms) / K
+    res = {
+        "metric": METRIC,
+        "value": round(graft_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": sh.dtype,
+        "data": "synthetic (seeded counter-hash generator; no benchmark items, no weights)",
+        "config": {
+            "workload": f"{w.name}: 7B-class GQA cache, {sh.n_layers} layers, {sh.n_q_heads}/{sh.n_kv_heads} heads, "
+                        f"head_dim {sh.head_dim}, {sh.dtype}; graft 1024-token prefix + 6 of "
+                        f"{len(w.lib_lengths) - 1} library segments (U[200,800] tokens); 64 patch tokens; "
+                        f"{w.n_decode} decode steps; batch 1",
+            "grafted_tokens_mean": round(float(np.mean([t.grafted_tokens for t, _ in marks])), 1),
+            "library_gb": round(int(w.lib_lengths.sum()) * sh.token_bytes / 1e9, 2),
+            "distinct_task_per_step": True,
+        },
+        "patch_attn": {"tflops": round(attn_tflops, 3), "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
+                       "kernel_us_per_layer": round(a_kms * 1e3 / (K * sh.n_layers), 2),
+                       "with_append_and_merge_tflops": round(prefill_tflops, 3),
+                       "with_append_and_merge_us_per_layer": round(p_kms * 1e3 / (K * sh.n_layers), 2),
+                       "call_us_per_layer": round(p_ms * 1e3 / (K * sh.n_layers), 2)},
+        "decode": {"gbs": round(decode_gbs, 2), "frac": round(decode_gbs / HBM_PEAK_GBS, 4),
+                   "kernel_us_per_layer_step": round(d_kms * 1e3 / n_dec_calls, 2),
+                   "call_us_per_layer_step": round(d_ms * 1e3 / n_dec_calls, 2)},
+        "graft_kernel_us": round(g_kms * 1e3 / K, 2),
+        "graft_call_us": round(g_ms * 1e3 / K, 2),
+        "wall_s_timed": round(t_wall, 3),
+        "timing": "achieved = algorithmic work / kernel time from HIP events the library records on the call's "
+                  "stream around its own kernels; *_call_* figures include host work and plan uploads",
+        "roofline": {"bound": "hbm", "kernel": "fcg graft_kernel", "achieved": round(graft_gbs, 2),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(graft_gbs / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("graft_7b_traffic.json"),
+                     "algorithmic_bytes_per_launch": int(round(g_bytes / K))},
+        "roofline_patch_attn": {"bound": "mfma", "kernel": "fcg attn_prefill_mfma_kernel",
+                                "achieved": round(attn_tflops, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
+                                "traffic": measured_traffic("prefill_7b_traffic.json"),
+                                "algorithmic_flops_per_launch": int(round(p_flops / (K * sh.n_layers)))},
+    }
+    if not args.no_cpu_baseline:
+        log("bench: timing the CPU oracle on a sample")
+        res["cpu_baseline"] = cpu_baseline(w, task_ws)
+    setup.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -176,6 +176,23 @@ fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int
 
 /* ------------------------------------------------------------- diagnostics */
 
+/* Kernel timing (measurement, not part of the method).  While enabled, every
+ * call on this cache records HIP events on its stream around its kernels:
+ *   FCG_TIME_GRAFT        the graft kernel of fcg_graft
+ *   FCG_TIME_PREFILL_ATTN the attention kernel of fcg_patch_prefill
+ *   FCG_TIME_PREFILL      all kernels of fcg_patch_prefill (append, attention, merge)
+ *   FCG_TIME_DECODE       all kernels of fcg_decode (attention, merge)
+ * Plan uploads and host work are outside the intervals.  fcg_cache_timing_read
+ * waits for the recorded events, returns the number of intervals and their
+ * summed duration in milliseconds for one kind, and forgets them.  enable = 0
+ * stops recording (recorded intervals stay readable). */
+#define FCG_TIME_GRAFT 0
+#define FCG_TIME_PREFILL_ATTN 1
+#define FCG_TIME_PREFILL 2
+#define FCG_TIME_DECODE 3
+fcg_status fcg_cache_timing(fcg_cache* cache, int32_t enable);
+fcg_status fcg_cache_timing_read(fcg_cache* cache, int32_t kind, int32_t* count, double* total_ms);
+
 const char* fcg_status_string(fcg_status s);
 const char* fcg_last_error(void);
 

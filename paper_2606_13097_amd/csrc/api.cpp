@@ -179,6 +179,12 @@ struct fcg_cache {
   size_t qws_bytes = 0;
   float* part = nullptr;
   size_t part_bytes = 0;
+  float* dpart = nullptr;     // decode split partials
+  size_t dpart_bytes = 0;
+  // kernel timing (fcg_cache_timing): recorded (start, end) event pairs per kind
+  bool timing = false;
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[4];
+  std::vector<hipEvent_t> ev_pool;
 
   fcg_cache(const fcg_model_desc& d, int32_t ns, int32_t mt, int32_t ps, int32_t np, uint32_t fl)
       : desc(d), n_seqs(ns), max_tokens(mt), page_size(ps), n_pages(np), flags(fl),
@@ -202,6 +208,34 @@ struct fcg_cache {
 };
 
 namespace {
+
+hipEvent_t timing_event(fcg_cache* c) {
+  if (!c->ev_pool.empty()) {
+    hipEvent_t e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+// Start an interval of `kind` on stream s (no-op unless timing is enabled).
+void time_begin(fcg_cache* c, int kind, hipStream_t s) {
+  if (!c->timing) return;
+  hipEvent_t a = timing_event(c);
+  if (!a) return;
+  hipEventRecord(a, s);
+  c->spans[kind].push_back({a, nullptr});
+}
+
+void time_end(fcg_cache* c, int kind, hipStream_t s) {
+  if (!c->timing || c->spans[kind].empty() || c->spans[kind].back().second) return;
+  hipEvent_t b = timing_event(c);
+  if (!b) return;
+  hipEventRecord(b, s);
+  c->spans[kind].back().second = b;
+}
 
 fcg_status grow(void** p, size_t* have, size_t need, const char* what) {
   if (need <= *have) return FCG_OK;
@@ -389,6 +423,7 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
       fcg_cache_destroy(c);
       return st;
     }
+
   }
   *out = c;
   return FCG_OK;
@@ -427,6 +462,34 @@ fcg_status fcg_cache_device_ptrs(const fcg_cache* c, int32_t layer, void** k, vo
   return FCG_OK;
 }
 
+fcg_status fcg_cache_timing(fcg_cache* c, int32_t enable) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  c->timing = enable != 0;
+  return FCG_OK;
+}
+
+fcg_status fcg_cache_timing_read(fcg_cache* c, int32_t kind, int32_t* count, double* total_ms) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (kind < 0 || kind > 3) return fail(FCG_ERANGE, "unknown timing kind");
+  double ms = 0.0;
+  int32_t n = 0;
+  for (auto& sp : c->spans[kind]) {
+    if (sp.second) {
+      HIP_TRY(hipEventSynchronize(sp.second), "hipEventSynchronize(timing)");
+      float t = 0.f;
+      HIP_TRY(hipEventElapsedTime(&t, sp.first, sp.second), "hipEventElapsedTime");
+      ms += t;
+      ++n;
+      c->ev_pool.push_back(sp.second);
+    }
+    c->ev_pool.push_back(sp.first);
+  }
+  c->spans[kind].clear();
+  if (count) *count = n;
+  if (total_ms) *total_ms = ms;
+  return FCG_OK;
+}
+
 fcg_status fcg_cache_destroy(fcg_cache* c) {
   if (!c) return FCG_OK;
   if (!c->layout_only()) {
@@ -439,6 +502,14 @@ fcg_status fcg_cache_destroy(fcg_cache* c) {
     if (c->d_inv_freq) hipFree(c->d_inv_freq);
     if (c->qws) hipFree(c->qws);
     if (c->part) hipFree(c->part);
+    if (c->dpart) hipFree(c->dpart);
+    for (auto& v : c->spans)
+      for (auto& sp : v) {
+        if (sp.first) hipEventDestroy(sp.first);
+        if (sp.second) hipEventDestroy(sp.second);
+      }
+    for (auto e : c->ev_pool) hipEventDestroy(e);
+
   }
   delete c;
   return FCG_OK;
@@ -484,8 +555,10 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   char* dev;
   size_t off;
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  time_begin(c, FCG_TIME_GRAFT, s);
   int rc = launch_graft(c->desc.dtype, (const GraftChunk*)(dev + o_chunks), (int)chunks.size(), lib->k, lib->v,
                         lib->cap, c->view(), c->d_inv_freq, c->desc.n_layers, s);
+  time_end(c, FCG_TIME_GRAFT, s);
   if (rc) return hip_fail((hipError_t)rc, "graft launch");
   if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
   for (auto& sp : spans) c->plan.mark_all_layers(sp.seq, sp.dst, sp.len);
@@ -513,11 +586,11 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     rblocks.push_back({r, u - r});
     r = u;
   }
-  // split the key range of each row block so that the grid fills the chip
+  // split the key range of each row block so that the grid covers the chip about once
   const int tile = mfma ? 64 : 256;
   int64_t total_tiles = 0;
   for (auto& rb : rblocks) total_tiles += (meta[rb.first + rb.second - 1].pos + tile) / tile;
-  const int64_t target = std::max<int64_t>(1, 512 / d.n_kv_heads);
+  const int64_t target = std::max<int64_t>(1, 256 / d.n_kv_heads);
   const int min_tiles = mfma ? 2 : 1;
   const int64_t per = std::max<int64_t>(min_tiles, (total_tiles + target - 1) / target);
   std::vector<AttnItem> items;
@@ -525,7 +598,8 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   int n_part = 0;
   for (auto& rb : rblocks) {
     const int kend = meta[rb.first + rb.second - 1].pos + 1;
-    const int64_t span = per * tile;
+    int64_t span = per * tile;
+    span = std::max<int64_t>(span, (kend + 255) / 256 + tile - 1) / tile * tile;  // at most 256 splits
     const int nsplit = (int)((kend + span - 1) / span);
     if (nsplit == 1) {
       items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, 0, kend, -1, 0, 0});
@@ -556,8 +630,11 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
   const TokenMeta* dmeta = (const TokenMeta*)(dev + o_meta);
   const CacheView cv = c->view();
+  const int tk_all = decode ? FCG_TIME_DECODE : FCG_TIME_PREFILL;
+  time_begin(c, tk_all, s);
   int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_inv_freq, d.n_q_heads, c->qws, s);
   if (rc) return hip_fail((hipError_t)rc, "append launch");
+  if (!decode) time_begin(c, FCG_TIME_PREFILL_ATTN, s);
   float* part_o = c->part;
   float* part_ml = c->part ? c->part + po : nullptr;
   if (mfma)
@@ -567,12 +644,95 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     rc = launch_attn_rows(d.dtype, (const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv,
                           layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
   if (rc) return hip_fail((hipError_t)rc, "attention launch");
+  if (!decode) time_end(c, FCG_TIME_PREFILL_ATTN, s);
   if (!comb.empty()) {
     rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), dmeta, d.n_q_heads,
                         d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s);
     if (rc) return hip_fail((hipError_t)rc, "combine launch");
   }
+  time_end(c, tk_all, s);
   return c->ring.retire(off, blob.bytes.size(), s);
+}
+
+// One decode launch per group of up to kMaxDecodeSeqs sequences, then one
+// combine launch for the sequences split over several blocks.  Split size:
+// enough blocks to cover the chip twice over, at least 128 keys (one chunk of
+// loads) per block.
+fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
+                      const void* q, const void* k, const void* v, void* out,
+                      const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
+  const fcg_model_desc& d = c->desc;
+  const int g = d.n_q_heads / d.n_kv_heads;
+  int64_t total = 0;
+  int32_t pmax = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    total += pos[i] + 1;
+    pmax = std::max(pmax, pos[i]);
+  }
+  const int64_t target_blocks = 512;
+  int64_t sk = (total * d.n_kv_heads + target_blocks - 1) / target_blocks;
+  sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);  // at most 256 splits per sequence (combine table)
+  sk = std::max<int64_t>(128, (sk + 127) / 128 * 128);
+  // partial slots: one per split of every multi-split sequence of a launch group
+  int max_slots = 0;
+  for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {
+    int slots = 0;
+    for (int32_t i = i0; i < std::min<int32_t>(n, i0 + kMaxDecodeSeqs); ++i) slots += (int)((pos[i] + sk) / sk);
+    max_slots = std::max(max_slots, slots);
+  }
+  const size_t po = (size_t)max_slots * d.n_kv_heads * g * d.head_dim, pml = (size_t)max_slots * d.n_kv_heads * g * 2;
+  if (fcg_status st = grow((void**)&c->dpart, &c->dpart_bytes, (po + pml) * sizeof(float), "decode partials"))
+    return st;
+  if (!new_pages.empty()) {
+    Blob blob;
+    std::vector<std::pair<int32_t, size_t>> rows;
+    stage_pages(c, new_pages, &blob, &rows);
+    char* dev;
+    size_t off;
+    if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+    if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
+  }
+  const CacheView cv = c->view();
+  const size_t es = esize(d.dtype);
+  float* part_o = c->dpart;
+  float* part_ml = c->dpart + po;
+  for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {
+    DecodeArgs a{};
+    a.n = std::min<int32_t>(kMaxDecodeSeqs, n - i0);
+    a.split_keys = (int32_t)sk;
+    a.split0[0] = 0;
+    std::vector<CombineItem> comb;
+    std::vector<TokenMeta> meta(a.n);
+    for (int32_t i = 0; i < a.n; ++i) {
+      a.seq[i] = seqs[i0 + i];
+      a.pos[i] = pos[i0 + i];
+      const int32_t ns = (int32_t)((pos[i0 + i] + sk) / sk);
+      a.split0[i + 1] = a.split0[i] + ns;
+      meta[i] = TokenMeta{i, seqs[i0 + i], pos[i0 + i], 0};
+      if (ns > 1) comb.push_back(CombineItem{i, 1, a.split0[i], ns});
+    }
+    const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
+    char* dev = nullptr;
+    size_t off = 0, o_meta = 0, o_comb = 0;
+    Blob blob;
+    if (!comb.empty()) {  // the merge plan goes up first so the two launches run back to back
+      o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
+      o_comb = blob.add(comb.data(), comb.size() * sizeof(CombineItem));
+      if (fcg_status st = upload(c, blob, {}, s, &dev, &off)) return st;
+    }
+    time_begin(c, FCG_TIME_DECODE, s);
+    int rc = launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv, layer,
+                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, s);
+    if (rc) return hip_fail((hipError_t)rc, "decode launch");
+    if (!comb.empty()) {
+      rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), (const TokenMeta*)(dev + o_meta),
+                          d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml, g, (char*)out + qoff, s);
+      if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
+      if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
+    }
+    time_end(c, FCG_TIME_DECODE, s);
+  }
+  return FCG_OK;
 }
 
 }  // namespace
@@ -616,9 +776,8 @@ fcg_status fcg_decode(fcg_cache* c, int32_t layer, int32_t n_seqs, const int32_t
   if (n_seqs == 0) return FCG_OK;
   if (!c->layout_only()) {
     HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
-    std::vector<TokenMeta> meta(n_seqs);
-    for (int32_t i = 0; i < n_seqs; ++i) meta[i] = TokenMeta{i, seqs[i], pos[i], 0};
-    if (fcg_status st = run_attention(c, layer, meta, true, q, k, v, out, new_pages, (hipStream_t)stream)) return st;
+    if (fcg_status st = run_decode(c, layer, n_seqs, seqs, pos, q, k, v, out, new_pages, (hipStream_t)stream))
+      return st;
   } else {
     c->plan.map_pages(new_pages);
   }

@@ -8,9 +8,10 @@
 //
 // Per tile of 64 keys:
 //   - the block stages K as rows [key][D] and V transposed [d][key] in LDS;
-//     waves 0-1 copy K vectors, waves 2-3 load 8x8 (key x dim) blocks of V and
-//     transpose them in registers, so every LDS write is a 16-byte vector.
-//     The next tile's global loads are issued before the current tile's math.
+//     every lane copies four K vectors and transposes one 4-key x 8-dim V
+//     block in registers (v_perm), so LDS writes are 16- and 8-byte vectors.
+//     The next tile's global loads are issued, unconditionally (positions
+//     clamped inside the split), before the current tile's math.
 //   - S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K from LDS, B = Q^T held
 //     in registers for the whole block).  In the accumulator layout lane l
 //     holds keys 4(l/16) .. +3 of a 16-key tile for query row l % 16, so each
@@ -32,6 +33,14 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(const uint4& u) { return __builtin_bit_cast(bf16x8_t, u); }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float float2_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> packed bf16 with the gfx950 conversion instruction (round to nearest even)
+__device__ __forceinline__ uint32_t cvt_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((float2_t){lo, hi}, bf16x2_t));
+}
+
 __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, const floatx4& c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
@@ -47,16 +56,15 @@ struct PrefillSmem {
   bf16_t vt[D * VROW];
 };
 
-template <int D>
+template <int D, bool PAGED>
 __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
     const AttnItem* __restrict__ items, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws,
     int rows_ws, CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int part_stride_rows) {
   constexpr int KS = D / 32;                 // 32-deep k steps over the head dimension
   constexpr int DT = D / 16;                 // 16-wide output tiles over the head dimension
-  constexpr int KVEC = kBN * D / 8;          // 16-byte vectors of a K tile
-  constexpr int KPT = KVEC / 128;            // per K-loading lane (lanes 0..127)
-  constexpr int VBLK = (kBN / 8) * (D / 8);  // 8x8 blocks of a V tile (lanes 128 .. 128 + VBLK - 1)
+  constexpr int KPT = kBN * D / 8 / 256;     // 16-byte K vectors per lane
+  constexpr int VBLK = (kBN / 4) * (D / 8);  // 4-key x 8-dim V blocks (lanes 0 .. VBLK - 1)
   using Sm = PrefillSmem<D>;
   __shared__ Sm sm;
 
@@ -70,68 +78,69 @@ __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
   const int rows = it.n_rank * g;
   const float qscale = 1.4426950408889634f / sqrtf((float)D);
 
-  // ---- query rows of this lane: one per 16-row tile
+  // ---- query rows of this lane: one per 16-row tile (rows past the block's
+  // last one load row 0 and are never written)
   int rpos[2];
   uint4 qf[2][KS];
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int r = 32 * w + 16 * rt + lr;
-    rpos[rt] = r < rows ? meta[it.rank0 + r / g].pos : -1;
+    const int rl = r < rows ? r : 0;
+    rpos[rt] = r < rows ? meta[it.rank0 + rl / g].pos : -1;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      qf[rt][ks] = r < rows ? ld16(qws + ((int64_t)hk * rows_ws + (int64_t)it.rank0 * g + r) * D + ks * 32 + lq * 8)
-                            : make_uint4(0, 0, 0, 0);
+      qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)it.rank0 * g + rl) * D + ks * 32 + lq * 8);
   }
   const int pmax = meta[it.rank0 + it.n_rank - 1].pos;
+  const int rmin = meta[it.rank0].pos;  // ranks ascend in position within a block
   const int kend = min(it.k1, pmax + 1);
 
   const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
   const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
 
-  // ---- tile loader state
-  uint4 pre[8];
+  // ---- tile loads: every lane KPT K vectors and (lanes < VBLK) one 4x8 V
+  // block; positions past the split are clamped to its last key, whose
+  // scores are masked, so every load is unconditional
+  uint4 kpre[KPT], vpre[4];
+  const int vkg = t % 16, vdc = t / 16;  // V block: keys 4 vkg .. +3, dims 8 vdc .. +7
+  // contiguous caches: one base per (layer, sequence, head), 32-bit offsets after
+  const int64_t head_base = PAGED ? 0 : kv_offset<false>(cv, layer, it.seq, hk, 0);
+  auto row_off = [&](int p) -> int64_t {
+    return PAGED ? kv_offset<true>(cv, layer, it.seq, hk, p) : head_base + (int64_t)(p * D);
+  };
   auto load_tile = [&](int kb) {
-    if (t < 128) {
 #pragma unroll
-      for (int i = 0; i < KPT; ++i) {
-        const int idx = i * 128 + t;
-        const int key = idx / (D / 8), c = idx % (D / 8);
-        const int p = kb + key;
-        pre[i] = p < kend ? ld16(ck + cache_offset(cv, layer, it.seq, hk, p) + c * 8) : make_uint4(0, 0, 0, 0);
-      }
-    } else if (t - 128 < VBLK) {
-      const int b = t - 128;
-      const int kg = b % (kBN / 8), dc = b / (kBN / 8);
+    for (int i = 0; i < KPT; ++i) {
+      const int idx = i * 256 + t;
+      const int key = idx / (D / 8), c = idx % (D / 8);
+      const int p = min(kb + key, kend - 1);
+      kpre[i] = ld16(ck + row_off(p) + c * 8);
+    }
+    if (VBLK == 256 || t < VBLK) {
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int p = kb + kg * 8 + i;
-        pre[i] = p < kend ? ld16(cvv + cache_offset(cv, layer, it.seq, hk, p) + dc * 8) : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < 4; ++i) {
+        const int p = min(kb + vkg * 4 + i, kend - 1);
+        vpre[i] = ld16(cvv + row_off(p) + vdc * 8);
       }
     }
   };
   auto store_tile = [&]() {
-    if (t < 128) {
 #pragma unroll
-      for (int i = 0; i < KPT; ++i) {
-        const int idx = i * 128 + t;
-        const int key = idx / (D / 8), c = idx % (D / 8);
-        st16(&sm.k[key * Sm::KROW + c * 8], pre[i]);
-      }
-    } else if (t - 128 < VBLK) {
-      const int b = t - 128;
-      const int kg = b % (kBN / 8), dc = b / (kBN / 8);
-      // pre[i] = V[key kg*8+i][dims dc*8 .. +7]; row e of the transpose = V[kg*8 .. +7][dc*8 + e]
-      const uint32_t* x = reinterpret_cast<const uint32_t*>(pre);  // x[4i + e/2], half e%2
+    for (int i = 0; i < KPT; ++i) {
+      const int idx = i * 256 + t;
+      const int key = idx / (D / 8), c = idx % (D / 8);
+      st16(&sm.k[key * Sm::KROW + c * 8], kpre[i]);
+    }
+    if (VBLK == 256 || t < VBLK) {
+      // vpre[i] = V[key 4 vkg + i][dims 8 vdc .. +7]; row e of the transpose holds
+      // V[4 vkg .. 4 vkg + 3][8 vdc + e]
+      const uint32_t* x = reinterpret_cast<const uint32_t*>(vpre);  // x[4i + e/2], half e%2
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        uint32_t wv[4];
-#pragma unroll
-        for (int i2 = 0; i2 < 4; ++i2) {
-          const uint32_t a = x[4 * (2 * i2) + e / 2], bb = x[4 * (2 * i2 + 1) + e / 2];
-          // low half: element e of key 2*i2; high half: element e of key 2*i2 + 1
-          wv[i2] = (e & 1) ? __builtin_amdgcn_perm(bb, a, 0x07060302u) : __builtin_amdgcn_perm(bb, a, 0x05040100u);
-        }
-        st16(&sm.vt[(dc * 8 + e) * Sm::VROW + kg * 8], make_uint4(wv[0], wv[1], wv[2], wv[3]));
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t w01 = __builtin_amdgcn_perm(x[4 + e / 2], x[e / 2], sel);
+        const uint32_t w23 = __builtin_amdgcn_perm(x[12 + e / 2], x[8 + e / 2], sel);
+        *reinterpret_cast<uint2*>(&sm.vt[(vdc * 8 + e) * Sm::VROW + vkg * 4]) = make_uint2(w01, w23);
       }
     }
   };
@@ -150,7 +159,11 @@ __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
     __syncthreads();
     store_tile();
     __syncthreads();
-    if (kb + kBN < kend) load_tile(kb + kBN);
+    load_tile(kb + kBN);  // past the end it re-reads the clamped last key: no branch, no stall
+    // keep the next tile's loads issued here, ahead of this tile's math (the
+    // compiler would otherwise sink them to their LDS stores and serialise
+    // memory latency with the matrix work)
+    __asm__ volatile("" ::: "memory");
 
     // S^T = K Q^T: four 16-key tiles x two 16-row tiles
     floatx4 st[2][4];
@@ -167,7 +180,9 @@ __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
         st[rt][kt] = c;
       }
     }
-    // mask, running max, probabilities
+    // mask (only tiles that reach past a row's position or the split's end),
+    // running max, probabilities
+    const bool need_mask = kb + kBN > kend || kb + kBN - 1 > rmin;
     uint4 pb[2][2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
@@ -176,35 +191,46 @@ __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const int p = kb + kt * 16 + lq * 4 + e;
-          const float sv = (p <= rpos[rt] && p < kend) ? st[rt][kt][e] * qscale : -INFINITY;
+          float sv = st[rt][kt][e] * qscale;
+          if (need_mask) {
+            const int p = kb + kt * 16 + lq * 4 + e;
+            sv = (p <= rpos[rt] && p < kend) ? sv : -INFINITY;
+          }
           st[rt][kt][e] = sv;
           tmax = fmaxf(tmax, sv);
         }
       tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
       tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
-      const float mnew = fmaxf(mrow[rt], tmax);
-      const float mref = mnew == -INFINITY ? 0.f : mnew;
-      const float alpha = exp2f(mrow[rt] - mref);
-      mrow[rt] = mnew;
+      // lazy rescale: the reference max moves only when a row's max grows by
+      // more than 2^8 (or on its first visible key); until then
+      // probabilities stay below 2^8, harmless in fp32 and in bf16
+      const bool grow = tmax > mrow[rt] + 8.f;
+      if (__builtin_amdgcn_ballot_w64(grow)) {  // wave-uniform: any row of the wave
+        const float mnew = fmaxf(mrow[rt], tmax);
+        const float mref = mnew == -INFINITY ? 0.f : mnew;
+        const float alpha = mrow[rt] == -INFINITY ? 0.f : exp2f(mrow[rt] - mref);
+        mrow[rt] = mnew;
+        lsum[rt] *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) acc[rt][dt] *= alpha;
+      }
+      const float mref = mrow[rt] == -INFINITY ? 0.f : mrow[rt];
       float ps = 0.f;
       float pv[4][4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          pv[kt][e] = exp2f(st[rt][kt][e] - mref);
+          pv[kt][e] = __builtin_amdgcn_exp2f(st[rt][kt][e] - mref);  // v_exp_f32: -inf gives 0
           ps += pv[kt][e];
         }
-      lsum[rt] = fmaf(lsum[rt], alpha, ps);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) acc[rt][dt] *= alpha;
+      lsum[rt] += ps;
       // B operand of step s (keys 32s .. 32s+31): tiles 2s (elements 0-3) and 2s+1 (elements 4-7)
 #pragma unroll
       for (int s = 0; s < 2; ++s)
-        pb[rt][s] = make_uint4(pack_bf16x2(pv[2 * s][0], pv[2 * s][1]), pack_bf16x2(pv[2 * s][2], pv[2 * s][3]),
-                               pack_bf16x2(pv[2 * s + 1][0], pv[2 * s + 1][1]),
-                               pack_bf16x2(pv[2 * s + 1][2], pv[2 * s + 1][3]));
+        pb[rt][s] = make_uint4(cvt_bf16x2(pv[2 * s][0], pv[2 * s][1]), cvt_bf16x2(pv[2 * s][2], pv[2 * s][3]),
+                               cvt_bf16x2(pv[2 * s + 1][0], pv[2 * s + 1][1]),
+                               cvt_bf16x2(pv[2 * s + 1][2], pv[2 * s + 1][3]));
     }
     // O^T += V^T P^T
 #pragma unroll
@@ -237,7 +263,7 @@ __global__ void __launch_bounds__(256) attn_prefill_mfma_kernel(
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 a = acc[rt][dt];
         *reinterpret_cast<uint2*>(o + dt * 16) =
-            make_uint2(pack_bf16x2(a[0] * inv, a[1] * inv), pack_bf16x2(a[2] * inv, a[3] * inv));
+            make_uint2(cvt_bf16x2(a[0] * inv, a[1] * inv), cvt_bf16x2(a[2] * inv, a[3] * inv));
       }
     } else {
       const int64_t pr = ((int64_t)it.part * Hkv + hk) * part_stride_rows + r;
@@ -260,12 +286,13 @@ int launch_attn_mfma(const AttnItem* items, int n_items, const TokenMeta* meta, 
                      int part_stride_rows, hipStream_t s) {
   if (n_items == 0) return 0;
   dim3 grid(n_items, cv.n_kv_heads);
-  if (cv.head_dim == 128)
-    hipLaunchKernelGGL((attn_prefill_mfma_kernel<128>), grid, dim3(256), 0, s, items, meta, (const bf16_t*)qws,
-                       rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows);
-  else
-    hipLaunchKernelGGL((attn_prefill_mfma_kernel<64>), grid, dim3(256), 0, s, items, meta, (const bf16_t*)qws,
-                       rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows);
+#define PF(DD, PG)                                                                                         \
+  hipLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG>), grid, dim3(256), 0, s, items, meta, (const bf16_t*)qws, \
+                     rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
+  const bool paged = cv.page_size != 0;
+  if (cv.head_dim == 128) { if (paged) PF(128, true); else PF(128, false); }
+  else { if (paged) PF(64, true); else PF(64, false); }
+#undef PF
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

@@ -155,36 +155,96 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
 }
 
 // Merge split-KV partials: per row, M = max M_s, L = sum L_s 2^(M_s - M),
-// O = sum O_s 2^(M_s - M) / L.  One block per (row block, kv head).
-template <typename T>
+// O = sum O_s 2^(M_s - M) / L.  Block (row block, kv head, z) merges up to
+// kCombRows rows: every lane first fetches one (M_s, L_s) pair into LDS (all
+// pairs in flight at once), the scale 2^(M_s - M) / L of every split is formed
+// there, then the 4-dim output chunks are summed over the splits with
+// 16-byte loads, LPC lanes per chunk taking interleaved splits, and the LPC
+// sums are added through LDS.
+constexpr int kCombRows = 8;
+constexpr int kCombMaxParts = 256;
+
+template <typename T, int D>
 __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restrict__ items,
-                                                      const TokenMeta* __restrict__ meta, int Hq, int Hkv, int D,
+                                                      const TokenMeta* __restrict__ meta, int Hq, int Hkv,
                                                       const float* __restrict__ part_o,
                                                       const float* __restrict__ part_ml, int part_stride_rows,
                                                       T* __restrict__ out) {
+  __shared__ float s_f[kCombRows][kCombMaxParts];
+  __shared__ float4 s_acc[256];
   const CombineItem it = items[blockIdx.x];
   const int hk = blockIdx.y;
   const int g = Hq / Hkv;
-  const int rows = it.n_rank * g;
-  for (int i = threadIdx.x; i < rows * D; i += blockDim.x) {
-    const int row = i / D, d = i % D;
+  const int t = threadIdx.x;
+  const int r0 = blockIdx.z * kCombRows;
+  const int nr = min(kCombRows, it.n_rank * g - r0);
+  if (nr <= 0) return;
+  const int np = it.n_part;
+  auto prow = [&](int s, int r) { return ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + r0 + r; };
+  for (int idx = t; idx < nr * np; idx += 256) {
+    const int r = idx / np, s = idx % np;
+    s_f[r][s] = part_ml[prow(s, r) * 2];
+  }
+  __syncthreads();
+  if (t < nr) {
     float M = -INFINITY;
-    for (int s = 0; s < it.n_part; ++s) {
-      const int64_t pr = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + row;
-      M = fmaxf(M, part_ml[pr * 2]);
+    for (int s = 0; s < np; ++s) M = fmaxf(M, s_f[t][s]);
+    float L = 0.f;
+    for (int s = 0; s < np; ++s) {
+      const float ms = s_f[t][s];
+      const float f = ms == -INFINITY ? 0.f : exp2f(ms - M);
+      s_f[t][s] = f;
+      L = fmaf(part_ml[prow(s, t) * 2 + 1], f, L);
     }
-    float L = 0.f, O = 0.f;
-    if (M != -INFINITY)
-      for (int s = 0; s < it.n_part; ++s) {
-        const int64_t pr = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + row;
-        const float ms = part_ml[pr * 2];
-        if (ms == -INFINITY) continue;
-        const float f = exp2f(ms - M);
-        L = fmaf(part_ml[pr * 2 + 1], f, L);
-        O = fmaf(part_o[pr * D + d], f, O);
-      }
-    const TokenMeta m = meta[it.rank0 + row / g];
-    Store<T>::store1(out + ((int64_t)m.tok * Hq + hk * g + row % g) * D + d, L > 0.f ? O / L : 0.f);
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    for (int s = 0; s < np; ++s) s_f[t][s] *= inv;
+  }
+  __syncthreads();
+  constexpr int CPR = D / 4;                  // 4-dim chunks per row
+  const int nch = nr * CPR;
+  const int lpc = max(1, 256 / nch);          // lanes per chunk (power of two: nr, CPR are)
+  for (int c = t / lpc; c < nch; c += 256 / lpc) {
+    const int sub = t % lpc;
+    const int r = c / CPR, c4 = c % CPR;
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll 8
+    for (int s = sub; s < np; s += lpc) {
+      const float f = s_f[r][s];
+      const float4 o = *reinterpret_cast<const float4*>(part_o + prow(s, r) * D + c4 * 4);
+      acc.x = fmaf(o.x, f, acc.x);
+      acc.y = fmaf(o.y, f, acc.y);
+      acc.z = fmaf(o.z, f, acc.z);
+      acc.w = fmaf(o.w, f, acc.w);
+    }
+    if (lpc > 1) {
+      s_acc[t] = acc;
+    } else {
+      const TokenMeta m = meta[it.rank0 + (r0 + r) / g];
+      T* dst = out + ((int64_t)m.tok * Hq + hk * g + (r0 + r) % g) * D + c4 * 4;
+      Store<T>::store1(dst + 0, acc.x);
+      Store<T>::store1(dst + 1, acc.y);
+      Store<T>::store1(dst + 2, acc.z);
+      Store<T>::store1(dst + 3, acc.w);
+    }
+  }
+  if (lpc == 1) return;
+  __syncthreads();
+  if (t < nch) {
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int sub = 0; sub < lpc; ++sub) {
+      const float4 a4 = s_acc[t * lpc + sub];
+      acc.x += a4.x;
+      acc.y += a4.y;
+      acc.z += a4.z;
+      acc.w += a4.w;
+    }
+    const int r = t / CPR, c4 = t % CPR;
+    const TokenMeta m = meta[it.rank0 + (r0 + r) / g];
+    T* dst = out + ((int64_t)m.tok * Hq + hk * g + (r0 + r) % g) * D + c4 * 4;
+    Store<T>::store1(dst + 0, acc.x);
+    Store<T>::store1(dst + 1, acc.y);
+    Store<T>::store1(dst + 2, acc.z);
+    Store<T>::store1(dst + 3, acc.w);
   }
 }
 
@@ -218,13 +278,13 @@ int launch_combine(int dtype, const CombineItem* items, int n_items, const Token
                    int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
                    hipStream_t s) {
   if (n_items == 0) return 0;
-  dim3 grid(n_items, Hkv);
-  if (dtype == 0)
-    hipLaunchKernelGGL((combine_kernel<float>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, D, part_o, part_ml,
-                       part_stride_rows, (float*)out);
-  else
-    hipLaunchKernelGGL((combine_kernel<bf16_t>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, D, part_o,
-                       part_ml, part_stride_rows, (bf16_t*)out);
+  dim3 grid(n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
+#define CB(T, DD)                                                                                            \
+  hipLaunchKernelGGL((combine_kernel<T, DD>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o, part_ml, \
+                     part_stride_rows, (T*)out)
+  if (dtype == 0) { if (D == 64) CB(float, 64); else CB(float, 128); }
+  else { if (D == 64) CB(bf16_t, 64); else CB(bf16_t, 128); }
+#undef CB
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

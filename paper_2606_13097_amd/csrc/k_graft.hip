@@ -64,22 +64,21 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
   T* ck = reinterpret_cast<T*>(cv.k);
   T* cvv = reinterpret_cast<T*>(cv.v);
 
-  // issue every load of the block first
+  // issue every load of the block first; rows past the run re-read its last
+  // row (their stores are skipped), so the loads carry no branches
   uint4 klo[KP], khi[KP], vv[VP];
   const int kc = t % KT, kr = t / KT;
 #pragma unroll
   for (int p = 0; p < KP; ++p) {
-    const int j = p * KR + kr;
-    if (j < ch.n) {
-      klo[p] = ld16(sk + (int64_t)j * D + kc * VEC);
-      khi[p] = ld16(sk + (int64_t)j * D + HALF + kc * VEC);
-    }
+    const int j = min(p * KR + kr, ch.n - 1);
+    klo[p] = ld16(sk + (int64_t)j * D + kc * VEC);
+    khi[p] = ld16(sk + (int64_t)j * D + HALF + kc * VEC);
   }
   const int vc = t % VT, vr = t / VT;
 #pragma unroll
   for (int p = 0; p < VP; ++p) {
-    const int j = p * VR + vr;
-    if (j < ch.n) vv[p] = ld16(sv + (int64_t)j * D + vc * VEC);
+    const int j = min(p * VR + vr, ch.n - 1);
+    vv[p] = ld16(sv + (int64_t)j * D + vc * VEC);
   }
   __syncthreads();  // cos/sin ready
 
@@ -101,7 +100,7 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
         y1[e] = fmaf(x1[e], c[e], -x2[e] * s[e]);
         y2[e] = fmaf(x2[e], c[e], x1[e] * s[e]);
       }
-      const int64_t off = cache_offset(cv, l, ch.seq, h, ch.dst + j);
+      const int64_t off = kv_offset<PAGED>(cv, l, ch.seq, h, ch.dst + j);
       st16(ck + off + kc * VEC, Store<T>::pack(y1));
       st16(ck + off + HALF + kc * VEC, Store<T>::pack(y2));
     }
@@ -110,7 +109,7 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
   for (int p = 0; p < VP; ++p) {
     const int j = p * VR + vr;
     if (j < ch.n) {
-      const int64_t off = cache_offset(cv, l, ch.seq, h, ch.dst + j);
+      const int64_t off = kv_offset<PAGED>(cv, l, ch.seq, h, ch.dst + j);
       st16(cvv + off + vc * VEC, vv[p]);
     }
   }

@@ -38,6 +38,16 @@ __host__ __device__ inline int64_t cache_offset(const CacheView& c, int layer, i
   return base + (((int64_t)page * c.n_kv_heads + head) * c.page_size + (pos % c.page_size)) * c.head_dim;
 }
 
+// Element offset of (layer, seq, head, pos) with the layout known at compile time.
+template <bool PAGED>
+__device__ __forceinline__ int64_t kv_offset(const CacheView& c, int layer, int seq, int head, int pos) {
+  if (PAGED) {
+    const int32_t page = c.page_table[(int64_t)seq * c.n_lp + (pos >> 4)];
+    return (int64_t)layer * c.layer_stride + (((int64_t)page * c.n_kv_heads + head) * 16 + (pos & 15)) * c.head_dim;
+  }
+  return (int64_t)layer * c.layer_stride + (((int64_t)seq * c.n_kv_heads + head) * c.max_tokens + pos) * c.head_dim;
+}
+
 // Per fresh (or decode) token, in attention order: tokens grouped by sequence,
 // ascending position inside a sequence.  Query rows of kv head h for the token
 // of rank r are r * g .. r * g + g - 1 of the query workspace.
@@ -63,6 +73,17 @@ struct CombineItem {
   int32_t part0, n_part;  // partial slots part0 .. part0 + n_part - 1
 };
 
+// By-value arguments of one fused decode launch (up to kMaxDecodeSeqs sequences).
+constexpr int kMaxDecodeSeqs = 64;
+struct DecodeArgs {
+  int32_t n;           // sequences in this launch
+  int32_t split_keys;  // key positions per split
+  int32_t pad0, pad1;
+  int32_t seq[kMaxDecodeSeqs];
+  int32_t pos[kMaxDecodeSeqs];         // the new token's position (= the sequence's length)
+  int32_t split0[kMaxDecodeSeqs + 1];  // first block of each sequence; split0[n] = grid size
+};
+
 int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len,
                       int Hkv, int D, int64_t cap, int64_t tok_off, hipStream_t s);
 
@@ -84,6 +105,14 @@ int launch_attn_mfma(const AttnItem* items, int n_items, const TokenMeta* meta, 
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
                      int rows_ws, const CacheView& cv, int layer, int Hq, void* out, float* part_o,
                      float* part_ml, int part_stride_rows, hipStream_t s);
+
+// Decode step: encode + store the new token and split-KV attention over the
+// cache.  q, k, v, out: [n][H][D] rows in the order of args.seq.  Splits of
+// multi-split sequences leave partials in part_o [slot][Hkv][g][D] and
+// part_ml [slot][Hkv][g][2], slot = split0[i] + split, for launch_combine.
+int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
+                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                  hipStream_t s);
 
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
                    int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,

@@ -34,7 +34,9 @@ EXPORTS = [
     "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
     "fcg_cache_create", "fcg_cache_reset", "fcg_cache_export_layout", "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
+    "fcg_cache_timing", "fcg_cache_timing_read",
 ]
+FCG_TIME_GRAFT, FCG_TIME_PREFILL_ATTN, FCG_TIME_PREFILL, FCG_TIME_DECODE = range(4)
 
 
 class FcgError(RuntimeError):
@@ -74,6 +76,8 @@ def _load():
         "fcg_graft": [P, P, I32, PI32, PI32, PI32, P],
         "fcg_patch_prefill": [P, I32, I32, PI32, PI32, P, P, P, P, P],
         "fcg_decode": [P, I32, I32, PI32, P, P, P, P, PI32, P],
+        "fcg_cache_timing": [P, I32],
+        "fcg_cache_timing_read": [P, I32, PI32, C.POINTER(C.c_double)],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -243,6 +247,17 @@ def fcg_decode(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.
     _check(_L.fcg_decode(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
                          pos.ctypes.data_as(C.POINTER(C.c_int32)), _stream(stream) if q is not None else None))
     return pos[:s.size]
+
+
+def fcg_cache_timing(cache: Cache, enable: bool) -> None:
+    _check(_L.fcg_cache_timing(cache.h, int(bool(enable))))
+
+
+def fcg_cache_timing_read(cache: Cache, kind: int):
+    """-> (number of recorded intervals, their summed duration in ms)."""
+    n, ms = C.c_int32(), C.c_double()
+    _check(_L.fcg_cache_timing_read(cache.h, int(kind), C.byref(n), C.byref(ms)))
+    return n.value, ms.value
 
 
 def fcg_status_string(status: int) -> str:

@@ -1,0 +1,98 @@
+"""Turn rocprofv3 CSV output into the short summaries kept under ``profiles/``.
+
+    python -m paper_2606_13097_amd.profiling stats KERNEL_STATS_CSV --title T --command C
+    python -m paper_2606_13097_amd.profiling traffic --kernel graft_kernel --source csrc/k_graft.hip \
+        --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv --copy-bytes 1073741824 \
+        --skip 1 --command C
+
+``traffic`` averages the kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) over its
+dispatches after the first ``--skip`` ones, and calibrates each counter by what it reads
+for a plain device copy of ``--copy-bytes`` bytes.  The JSON records the SHA-256 of the
+kernel's source file: ``bench.py`` reports the traffic only while that source is unchanged.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+
+
+def source_sha256(rel: str) -> str:
+    with open(os.path.join(PKG, rel), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def _short(name: str) -> str:
+    n = name.replace("void ", "")
+    depth, out = 0, []
+    for ch in n:  # cut the argument list, keep template arguments
+        if ch == "(" and depth == 0:
+            break
+        depth += ch == "<"
+        depth -= ch == ">"
+        out.append(ch)
+    return "".join(out).strip() or name[:40]
+
+
+def stats_markdown(path: str, title: str, command: str) -> str:
+    rows = list(csv.DictReader(open(path)))
+    lines = [f"# {title}", "", "Command:", "", f"    {command}", "",
+             "| kernel | calls | avg (us) | min (us) | max (us) | total (ms) |", "|---|---|---|---|---|---|"]
+    for r in rows:
+        lines.append(f"| {_short(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
+    return "\n".join(lines) + "\n"
+
+
+def _per_dispatch(path: str, kernel: str, counter: str):
+    vals = []
+    for r in csv.DictReader(open(path)):
+        if kernel in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            vals.append((int(r["Dispatch_Id"]), float(r["Counter_Value"])))
+    return [v for _, v in sorted(vals)]
+
+
+def traffic(args) -> dict:
+    f = _per_dispatch(args.fetch, args.kernel, "FETCH_SIZE")[args.skip:]
+    w = _per_dispatch(args.write, args.kernel, "WRITE_SIZE")[args.skip:]
+    cf = max(v for v in _per_dispatch(args.copy_fetch, args.copy_kernel, "FETCH_SIZE"))
+    cw = max(v for v in _per_dispatch(args.copy_write, args.copy_kernel, "WRITE_SIZE"))
+    ff = args.copy_bytes / (cf * 1024.0)
+    wf = args.copy_bytes / (cw * 1024.0)
+    fetch_b = sum(f) / len(f) * 1024.0 * ff
+    write_b = sum(w) / len(w) * 1024.0 * wf
+    return {"kernel": args.kernel, "source": args.source, "source_sha256": source_sha256(args.source),
+            "dispatches": len(f), "fetch_kib_avg": sum(f) / len(f), "write_kib_avg": sum(w) / len(w),
+            "fetch_factor": ff, "write_factor": wf, "traffic_bytes_per_launch": fetch_b + write_b,
+            "command": args.command}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("--title", required=True)
+    s.add_argument("--command", required=True)
+    t = sub.add_parser("traffic")
+    for k in ("kernel", "source", "fetch", "write", "copy_fetch", "copy_write", "command"):
+        t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    t.add_argument("--copy-kernel", default="copyBuffer")
+    t.add_argument("--copy-bytes", type=float, default=float(1 << 30))
+    t.add_argument("--skip", type=int, default=0)
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        sys.stdout.write(stats_markdown(a.csv, a.title, a.command))
+    else:
+        json.dump(traffic(a), sys.stdout, indent=1)
+        sys.stdout.write("\n")
+
+
+if __name__ == "__main__":
+    main()

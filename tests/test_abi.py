@@ -43,3 +43,15 @@ def test_status_strings_and_errors_without_gpu():
         fcg.Cache(fcg.model_desc(1, 4, 2, 64, 1e4, "bf16"), 1, 16, page_size=8, n_pages=4,
                   flags=fcg.FCG_LAYOUT_ONLY)
     assert e.value.status == fcg.FCG_EINVAL
+
+
+def test_timing_api_without_device_work():
+    from paper_2606_13097_amd import fcg
+    c = fcg.Cache(fcg.model_desc(1, 4, 2, 64, 1e4, "f32"), 1, 32, flags=fcg.FCG_LAYOUT_ONLY)
+    fcg.fcg_cache_timing(c, True)
+    fcg.fcg_patch_prefill(c, 0, [0, 0], [0, 1], None, None, None, None)
+    for kind in range(4):
+        assert fcg.fcg_cache_timing_read(c, kind) == (0, 0.0)
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.fcg_cache_timing_read(c, 4)
+    assert e.value.status == fcg.FCG_ERANGE

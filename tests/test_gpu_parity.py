@@ -285,3 +285,25 @@ def test_synth_gpu_twin_matches_host_bits():
         sg.fill_rows(t, dt, 7, tag, 3, 11, 5, 0.5, rate)
         ref = synth.tensor_values(7, tag, 3, 11, np.arange(5, 42), 8, 128, 0.5, dt, rate)
         np.testing.assert_array_equal(storage_np(t), ref)
+
+
+def test_kernel_timing_counts_calls():
+    from paper_2606_13097_amd import fcg, runner, synth
+    w = synth.workload("7b", seed=6, n_layers=2, n_lib=8)
+    say("[gpu] timing")
+    s = runner.GpuSetup(w)
+    try:
+        fcg.fcg_cache_timing(s.cache, True)
+        s.graft()
+        for layer in range(2):
+            q, k, v = s.fresh_inputs(layer)
+            s.prefill(layer, q, k, v, torch.empty_like(q))
+        dq, dk, dv = s.decode_inputs(0, 3)
+        for t in range(3):
+            s.decode(0, dq[t], dk[t], dv[t], torch.empty_like(dq[t]))
+        counts = [fcg.fcg_cache_timing_read(s.cache, k) for k in range(4)]
+        assert [c[0] for c in counts] == [1, 2, 2, 3]
+        assert all(c[1] > 0 for c in counts)
+        assert counts[2][1] >= counts[1][1]            # the whole prefill includes its attention kernel
+    finally:
+        s.close()
