@@ -577,8 +577,8 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   const int n = (int)meta.size();
   const int g = d.n_q_heads / d.n_kv_heads;
   const bool mfma = !decode && d.dtype == FCG_BF16;
-  // row blocks: consecutive ranks of one sequence, at most 128 query rows (MFMA) or one token
-  const int max_rank = mfma ? std::max(1, 128 / g) : 1;
+  // row blocks: consecutive ranks of one sequence, at most 256 query rows (MFMA) or one token
+  const int max_rank = mfma ? std::max(1, 256 / g) : 1;
   std::vector<std::pair<int, int>> rblocks;  // (rank0, n_rank)
   for (int r = 0; r < n;) {
     int u = r;
@@ -593,25 +593,61 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   const int64_t target = std::max<int64_t>(1, 256 / d.n_kv_heads);
   const int min_tiles = mfma ? 2 : 1;
   const int64_t per = std::max<int64_t>(min_tiles, (total_tiles + target - 1) / target);
-  std::vector<AttnItem> items;
+  // one split length for the call (at most 256 splits per row block: the merge table)
+  int64_t span = per * tile;
+  for (auto& rb : rblocks) {
+    const int kend = meta[rb.first + rb.second - 1].pos + 1;
+    span = std::max<int64_t>(span, ((kend + 255) / 256 + tile - 1) / tile * tile);
+  }
+  std::vector<AttnItem> items;                 // VALU path: one item per (row block, split)
+  std::vector<PrefillRb> pf_rb;                // MFMA path: row blocks, items built per launch
+  std::vector<int> pf_nsplit;
   std::vector<CombineItem> comb;
   int n_part = 0;
   for (auto& rb : rblocks) {
     const int kend = meta[rb.first + rb.second - 1].pos + 1;
-    int64_t span = per * tile;
-    span = std::max<int64_t>(span, (kend + 255) / 256 + tile - 1) / tile * tile;  // at most 256 splits
     const int nsplit = (int)((kend + span - 1) / span);
-    if (nsplit == 1) {
-      items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, 0, kend, -1, 0, 0});
-    } else {
-      comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit});
-      for (int sidx = 0; sidx < nsplit; ++sidx)
-        items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, (int)(sidx * span),
-                                 (int)std::min<int64_t>(kend, (sidx + 1) * span), n_part + sidx, 0, 0});
-      n_part += nsplit;
+    const int part0 = nsplit > 1 ? n_part : -1;
+    if (nsplit > 1) comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit});
+    pf_rb.push_back(PrefillRb{rb.first, rb.second, meta[rb.first].seq, meta[rb.first].pos, kend - 1, part0});
+    pf_nsplit.push_back(nsplit);
+    for (int sidx = 0; sidx < nsplit; ++sidx)
+      items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, (int)(sidx * span),
+                               (int)std::min<int64_t>(kend, (sidx + 1) * span), nsplit > 1 ? n_part + sidx : -1, 0, 0});
+    if (nsplit > 1) n_part += nsplit;
+  }
+  // MFMA launches: up to kPfMaxRb row blocks and kPfMaxItems items each, items
+  // ordered (sequence, split, row block) so that the row blocks sharing a key
+  // split are neighbours (the kernel maps neighbours of a head to one XCD)
+  std::vector<PrefillArgs> pf_launch;
+  if (mfma) {
+    for (size_t b0 = 0; b0 < pf_rb.size();) {
+      PrefillArgs a{};
+      a.span = (int32_t)span;
+      size_t b1 = b0;
+      int n_it = 0;
+      while (b1 < pf_rb.size() && (int)(b1 - b0) < kPfMaxRb && n_it + pf_nsplit[b1] <= kPfMaxItems) n_it += pf_nsplit[b1++];
+      if (b1 == b0) return fail(FCG_EINVAL, "a row block needs more splits than one launch holds");
+      a.n_rb = (int32_t)(b1 - b0);
+      for (size_t b = b0; b < b1; ++b) a.rb[b - b0] = pf_rb[b];
+      int max_split = 0;
+      for (size_t b = b0; b < b1; ++b) max_split = std::max(max_split, pf_nsplit[b]);
+      for (size_t b = b0; b < b1;) {  // one sequence at a time
+        size_t e = b;
+        while (e < b1 && pf_rb[e].seq == pf_rb[b].seq) ++e;
+        for (int sp = 0; sp < max_split; ++sp)
+          for (size_t r = b; r < e; ++r)
+            if (sp < pf_nsplit[r]) a.item[a.n_items++] = (uint32_t)(r - b0) | ((uint32_t)sp << 8);
+        b = e;
+      }
+      pf_launch.push_back(a);
+      b0 = b1;
     }
   }
-  const int stride_rows = mfma ? 128 : g;
+  // MFMA blocks of 8 waves (256 rows) when some row block needs more than 4 waves
+  int max_rows = 0;
+  for (auto& rb : rblocks) max_rows = std::max(max_rows, rb.second * g);
+  const int stride_rows = mfma ? (max_rows > 128 ? 256 : 128) : g;
   // workspaces first: a failure here leaves the layout untouched
   const size_t qbytes = (size_t)d.n_kv_heads * n * g * d.head_dim * esize(d.dtype);
   if (fcg_status st = grow(&c->qws, &c->qws_bytes, qbytes, "query workspace")) return st;
@@ -623,7 +659,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   std::vector<std::pair<int32_t, size_t>> rows;
   stage_pages(c, new_pages, &blob, &rows);
   const size_t o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
-  const size_t o_items = blob.add(items.data(), items.size() * sizeof(AttnItem));
+  const size_t o_items = mfma ? 0 : blob.add(items.data(), items.size() * sizeof(AttnItem));
   const size_t o_comb = blob.add(comb.data(), comb.size() * sizeof(CombineItem));
   char* dev;
   size_t off;
@@ -637,17 +673,19 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   if (!decode) time_begin(c, FCG_TIME_PREFILL_ATTN, s);
   float* part_o = c->part;
   float* part_ml = c->part ? c->part + po : nullptr;
-  if (mfma)
-    rc = launch_attn_mfma((const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv, layer,
-                          d.n_q_heads, out, part_o, part_ml, stride_rows, s);
-  else
+  if (mfma) {
+    for (const PrefillArgs& a : pf_launch) {
+      rc = launch_attn_mfma(a, dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
+      if (rc) break;
+    }
+  } else
     rc = launch_attn_rows(d.dtype, (const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv,
                           layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
   if (rc) return hip_fail((hipError_t)rc, "attention launch");
   if (!decode) time_end(c, FCG_TIME_PREFILL_ATTN, s);
   if (!comb.empty()) {
     rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), dmeta, d.n_q_heads,
-                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s);
+                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s, mfma);
     if (rc) return hip_fail((hipError_t)rc, "combine launch");
   }
   time_end(c, tk_all, s);

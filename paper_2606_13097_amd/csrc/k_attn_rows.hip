@@ -164,7 +164,7 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
 constexpr int kCombRows = 8;
 constexpr int kCombMaxParts = 256;
 
-template <typename T, int D>
+template <typename T, int D, bool PART_BF16>
 __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restrict__ items,
                                                       const TokenMeta* __restrict__ meta, int Hq, int Hkv,
                                                       const float* __restrict__ part_o,
@@ -210,7 +210,13 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restr
 #pragma unroll 8
     for (int s = sub; s < np; s += lpc) {
       const float f = s_f[r][s];
-      const float4 o = *reinterpret_cast<const float4*>(part_o + prow(s, r) * D + c4 * 4);
+      float4 o;
+      if (PART_BF16) {
+        const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const bf16_t*>(part_o) + prow(s, r) * D + c4 * 4);
+        o = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
+      } else {
+        o = *reinterpret_cast<const float4*>(part_o + prow(s, r) * D + c4 * 4);
+      }
       acc.x = fmaf(o.x, f, acc.x);
       acc.y = fmaf(o.y, f, acc.y);
       acc.z = fmaf(o.z, f, acc.z);
@@ -276,12 +282,16 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq, int Hkv,
                    int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s) {
+                   hipStream_t s, bool part_bf16) {
   if (n_items == 0) return 0;
   dim3 grid(n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
 #define CB(T, DD)                                                                                            \
-  hipLaunchKernelGGL((combine_kernel<T, DD>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o, part_ml, \
-                     part_stride_rows, (T*)out)
+  if (part_bf16)                                                                                             \
+    hipLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o,   \
+                       part_ml, part_stride_rows, (T*)out);                                                  \
+  else                                                                                                       \
+    hipLaunchKernelGGL((combine_kernel<T, DD, false>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o,  \
+                       part_ml, part_stride_rows, (T*)out)
   if (dtype == 0) { if (D == 64) CB(float, 64); else CB(float, 128); }
   else { if (D == 64) CB(bf16_t, 64); else CB(bf16_t, 128); }
 #undef CB

@@ -96,8 +96,24 @@ int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, c
                        const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws,
                        hipStream_t s);
 
+// By-value work list of one MFMA prefill launch: row blocks (up to 128 query
+// rows of one sequence) and items (row block, key split of `span` positions),
+// so a block's first loads need no metadata round trip.
+constexpr int kPfMaxRb = 48;
+constexpr int kPfMaxItems = 512;
+struct PrefillRb {
+  int32_t rank0, n_rank, seq;
+  int32_t rmin, pmax;  // smallest and largest query position of the block
+  int32_t part0;       // first partial slot, -1 when the block has a single split
+};
+struct PrefillArgs {
+  int32_t n_rb, n_items, span, pad;
+  PrefillRb rb[kPfMaxRb];
+  uint32_t item[kPfMaxItems];  // row block | split << 8
+};
+
 // bf16 MFMA attention of query-workspace rows over the cache.
-int launch_attn_mfma(const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws, int rows_ws,
+int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
                      int part_stride_rows, hipStream_t s);
 
@@ -114,8 +130,9 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
                   hipStream_t s);
 
+// Merge split partials (part_o fp32, or bf16 when part_bf16) into out.
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
                    int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s);
+                   hipStream_t s, bool part_bf16 = false);
 
 }  // namespace fcg
