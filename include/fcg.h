@@ -116,7 +116,9 @@ fcg_status fcg_lib_destroy(fcg_lib* lib);
  * p / 16 of a sequence is mapped on first write to the lowest-numbered free
  * page, new pages of one call in ascending (sequence, logical page) order.
  * With FCG_LAYOUT_ONLY no device memory is allocated and graft, prefill
- * and decode only validate and record the layout (planning and tests). */
+ * and decode only validate and record the layout (planning and tests).
+ * Errors: EINVAL (bad descriptor, n_seqs or max_tokens < 1, max_tokens *
+ * head_dim >= 2^31, page_size not 0 or 16, unknown flags), ENOMEM, EHIP. */
 fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t max_tokens,
                             int32_t page_size, int32_t n_pages, uint32_t flags, fcg_cache** out);
 

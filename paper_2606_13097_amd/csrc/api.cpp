@@ -399,6 +399,8 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
   if (!out) return fail(FCG_EINVAL, "null output handle");
   if (fcg_status st = check_desc(desc)) return st;
   if (n_seqs < 1 || max_tokens < 1) return fail(FCG_EINVAL, "n_seqs and max_tokens must be >= 1");
+  if ((int64_t)max_tokens * desc->head_dim >= ((int64_t)1 << 31))
+    return fail(FCG_EINVAL, "max_tokens * head_dim must stay below 2^31");
   if (page_size != 0 && page_size != 16) return fail(FCG_EINVAL, "page_size must be 0 (contiguous) or 16");
   if (page_size && n_pages < 1) return fail(FCG_EINVAL, "a paged cache needs n_pages >= 1");
   if (flags & ~FCG_LAYOUT_ONLY) return fail(FCG_EINVAL, "unknown flags");
@@ -616,29 +618,18 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
                                (int)std::min<int64_t>(kend, (sidx + 1) * span), nsplit > 1 ? n_part + sidx : -1, 0, 0});
     if (nsplit > 1) n_part += nsplit;
   }
-  // MFMA launches: up to kPfMaxRb row blocks and kPfMaxItems items each, items
-  // ordered (sequence, split, row block) so that the row blocks sharing a key
-  // split are neighbours (the kernel maps neighbours of a head to one XCD)
+  // MFMA launches: up to kPfMaxRb row blocks each, every row block given the
+  // launch's largest split count (the extra splits are empty blocks)
   std::vector<PrefillArgs> pf_launch;
   if (mfma) {
     for (size_t b0 = 0; b0 < pf_rb.size();) {
       PrefillArgs a{};
       a.span = (int32_t)span;
-      size_t b1 = b0;
-      int n_it = 0;
-      while (b1 < pf_rb.size() && (int)(b1 - b0) < kPfMaxRb && n_it + pf_nsplit[b1] <= kPfMaxItems) n_it += pf_nsplit[b1++];
-      if (b1 == b0) return fail(FCG_EINVAL, "a row block needs more splits than one launch holds");
+      const size_t b1 = std::min(pf_rb.size(), b0 + (size_t)kPfMaxRb);
       a.n_rb = (int32_t)(b1 - b0);
-      for (size_t b = b0; b < b1; ++b) a.rb[b - b0] = pf_rb[b];
-      int max_split = 0;
-      for (size_t b = b0; b < b1; ++b) max_split = std::max(max_split, pf_nsplit[b]);
-      for (size_t b = b0; b < b1;) {  // one sequence at a time
-        size_t e = b;
-        while (e < b1 && pf_rb[e].seq == pf_rb[b].seq) ++e;
-        for (int sp = 0; sp < max_split; ++sp)
-          for (size_t r = b; r < e; ++r)
-            if (sp < pf_nsplit[r]) a.item[a.n_items++] = (uint32_t)(r - b0) | ((uint32_t)sp << 8);
-        b = e;
+      for (size_t b = b0; b < b1; ++b) {
+        a.rb[b - b0] = pf_rb[b];
+        a.n_split = std::max(a.n_split, pf_nsplit[b]);
       }
       pf_launch.push_back(a);
       b0 = b1;
@@ -693,9 +684,10 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
 }
 
 // One decode launch per group of up to kMaxDecodeSeqs sequences, then one
-// combine launch for the sequences split over several blocks.  Split size:
-// enough blocks to cover the chip twice over, at least 128 keys (one chunk of
-// loads) per block.
+// merge launch for the sequences split over several blocks; both take their
+// plan by value, so a decode step uploads nothing (new pages aside).  Split
+// size: enough blocks to cover the chip twice over, at least 128 keys per
+// block.
 fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
                       const void* q, const void* k, const void* v, void* out,
                       const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
@@ -739,35 +731,20 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     a.n = std::min<int32_t>(kMaxDecodeSeqs, n - i0);
     a.split_keys = (int32_t)sk;
     a.split0[0] = 0;
-    std::vector<CombineItem> comb;
-    std::vector<TokenMeta> meta(a.n);
     for (int32_t i = 0; i < a.n; ++i) {
       a.seq[i] = seqs[i0 + i];
       a.pos[i] = pos[i0 + i];
       const int32_t ns = (int32_t)((pos[i0 + i] + sk) / sk);
       a.split0[i + 1] = a.split0[i] + ns;
-      meta[i] = TokenMeta{i, seqs[i0 + i], pos[i0 + i], 0};
-      if (ns > 1) comb.push_back(CombineItem{i, 1, a.split0[i], ns});
+      a.max_split = std::max(a.max_split, ns);
     }
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
-    char* dev = nullptr;
-    size_t off = 0, o_meta = 0, o_comb = 0;
-    Blob blob;
-    if (!comb.empty()) {  // the merge plan goes up first so the two launches run back to back
-      o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
-      o_comb = blob.add(comb.data(), comb.size() * sizeof(CombineItem));
-      if (fcg_status st = upload(c, blob, {}, s, &dev, &off)) return st;
-    }
     time_begin(c, FCG_TIME_DECODE, s);
     int rc = launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv, layer,
                            c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, s);
     if (rc) return hip_fail((hipError_t)rc, "decode launch");
-    if (!comb.empty()) {
-      rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), (const TokenMeta*)(dev + o_meta),
-                          d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml, g, (char*)out + qoff, s);
-      if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
-      if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
-    }
+    rc = launch_decode_combine(d.dtype, a, d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml, (char*)out + qoff, s);
+    if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
     time_end(c, FCG_TIME_DECODE, s);
   }
   return FCG_OK;

@@ -8,7 +8,7 @@
 // split [k0, k1) of the key positions.  Wave w owns rows 32w .. 32w + 31 as
 // two 16-row tiles.
 //
-// The block stages up to 4 tiles of 64 keys at once: every load of the round
+// The block stages 2 or 4 tiles of 64 keys at once: every load of the round
 // is issued before any LDS write (one memory latency per round instead of one
 // per tile), K as rows [key][D], V transposed [d][key] (each lane transposes
 // 4-key x 8-dim blocks in registers with v_perm).  Then per tile, with no
@@ -46,41 +46,53 @@ __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
-constexpr int kBN = 64;          // keys per tile
-constexpr int kStageTiles = 4;   // tiles of a split staged in LDS at once
+constexpr int kBN = 64;  // keys per tile
 
 template <int D>
 struct PrefillTile {
-  static constexpr int KROW = D + 8;     // bf16 elements per staged K row (16-byte pad)
-  static constexpr int VROW = kBN + 8;   // bf16 elements per staged V^T row
+  // Row pitches chosen for conflict-free LDS reads: a 16-byte K read by 8
+  // lanes of 8 rows covers banks 4r .. 4r + 3 (pitch 68 dwords), an 8-byte
+  // V^T read by 16 lanes of 16 rows covers banks 2r, 2r + 1 (pitch 34 dwords).
+  static constexpr int KROW = D + 8;     // bf16 elements per staged K row
+  static constexpr int VROW = kBN + 4;   // bf16 elements per staged V^T row
   bf16_t k[kBN * KROW];
   bf16_t vt[D * VROW];
 };
 
-template <int D, bool PAGED, int WAVES>
+// grid (row block, key split, kv head); STAGE tiles of the split are staged
+// per round
+template <int D, bool PAGED, int WAVES, int STAGE>
 __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int part_stride_rows) {
-  constexpr int NT = WAVES * 64;             // lanes per block
-  constexpr int KS = D / 32;                 // 32-deep k steps over the head dimension
-  constexpr int DT = D / 16;                 // 16-wide output tiles over the head dimension
-  constexpr int KV = kBN * D / 8;            // 16-byte K vectors per tile
-  constexpr int VB = (kBN / 4) * (D / 8);    // 4-key x 8-dim V blocks per tile
-  constexpr int KPT = (kStageTiles * KV + NT - 1) / NT;  // staged K vectors per lane
-  constexpr int VPT = (kStageTiles * VB + NT - 1) / NT;  // staged V blocks per lane
+  constexpr int NT = WAVES * 64;                    // lanes per block
+  constexpr int KS = D / 32;                        // 32-deep k steps over the head dimension
+  constexpr int DT = D / 16;                        // 16-wide output tiles over the head dimension
+  constexpr int KV = kBN * D / 8;                   // 16-byte K vectors per tile
+  constexpr int VB = (kBN / 4) * (D / 8);           // 4-key x 8-dim V blocks per tile
+  constexpr int KPT = (STAGE * KV + NT - 1) / NT;   // staged K vectors per lane
+  constexpr int VPT = (STAGE * VB + NT - 1) / NT;   // staged V blocks per lane
   using Tile = PrefillTile<D>;
-  __shared__ Tile tiles[kStageTiles];
+  __shared__ Tile tiles[STAGE];
 
-  const uint32_t itm = args.item[blockIdx.x];
-  const PrefillRb rb = args.rb[itm & 0xFF];
-  const int split = (int)(itm >> 8);
-  const int hk = blockIdx.y;
+  const PrefillRb rb = args.rb[blockIdx.x];
+  const int split = blockIdx.y;
+  const int hk = blockIdx.z;
   const int Hkv = cv.n_kv_heads;
   const int k0 = split * args.span;
   const int kend = min(rb.pmax + 1, k0 + args.span);
   const int part = rb.part0 < 0 ? -1 : rb.part0 + split;
-  if (k0 >= kend) return;  // padding item of a shorter row block
+  const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
+  const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
+  // Every kernel argument the block reads, fetched in one batch of scalar
+  // loads before the first branch: left to the compiler, the loads are placed
+  // next to their uses and each costs a memory round trip of its own.
+  asm volatile("" ::"s"(rb.rank0), "s"(rb.n_rank), "s"(rb.seq), "s"(rb.rmin), "s"(kend), "s"(part), "s"(meta),
+               "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(Hkv),
+               "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
+  if (k0 >= kend) return;  // padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
   const int w = t >> 6, lane = t & 63;
@@ -90,23 +102,29 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 
   // query rows of this lane: one per 16-row tile (rows past the block's last
   // one load row 0 and are never written)
-  int rpos[2];
+  int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
   uint4 qf[2][KS];
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int r = 32 * w + 16 * rt + lr;
     const int rl = r < rows ? r : 0;
-    rpos[rt] = r < rows ? meta[rb.rank0 + rl / g].pos : -1;
+    const TokenMeta m = meta[rb.rank0 + rl / g];
+    rpos[rt] = m.pos;
+    rtok[rt] = m.tok;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
       qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)rb.rank0 * g + rl) * D + ks * 32 + lq * 8);
   }
 
-  const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
-  const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
+  // contiguous caches address a head's rows from one base with 32-bit offsets
   const int64_t head_base = PAGED ? 0 : kv_offset<false>(cv, layer, rb.seq, hk, 0);
-  auto row_off = [&](int p) -> int64_t {
-    return PAGED ? kv_offset<true>(cv, layer, rb.seq, hk, p) : head_base + (int64_t)(p * D);
+  const bf16_t* kbase = ck + head_base;
+  const bf16_t* vbase = cvv + head_base;
+  auto krow = [&](int p) -> const bf16_t* {
+    return PAGED ? ck + kv_offset<true>(cv, layer, rb.seq, hk, p) : kbase + p * D;
+  };
+  auto vrow = [&](int p) -> const bf16_t* {
+    return PAGED ? cvv + kv_offset<true>(cv, layer, rb.seq, hk, p) : vbase + p * D;
   };
 
   float mrow[2] = {-INFINITY, -INFINITY};
@@ -117,52 +135,47 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kr0 = k0; kr0 < kend; kr0 += kStageTiles * kBN) {
-    const int nt = min(kStageTiles, (kend - kr0 + kBN - 1) / kBN);  // tiles of this round
-    // ---- issue every load of the round, then stage it (positions past the
-    // split are clamped to its last key: valid memory, scores masked)
+  for (int kr0 = k0; kr0 < kend; kr0 += STAGE * kBN) {
+    const int nt = min(STAGE, (kend - kr0 + kBN - 1) / kBN);  // tiles of this round
+    // ---- issue every load of the round, then stage it.  Loads and LDS
+    // writes are unconditional: slots past the round's last tile repeat that
+    // tile (the same bytes to the same LDS addresses), and positions past the
+    // split are clamped to its last key (valid memory, scores masked).  A
+    // conditional load would make the compiler wait, in the next round, for
+    // loads it cannot prove complete before reusing their registers.
     uint4 kreg[KPT], vreg[VPT][4];
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int idx = i * NT + t;  // (tile, key, 16-byte chunk)
-      if (idx < nt * KV) {
-        const int tl = idx / KV, key = (idx % KV) / (D / 8), c = idx % (D / 8);
-        kreg[i] = ld16(ck + row_off(min(kr0 + tl * kBN + key, kend - 1)) + c * 8);
-      }
+      const int tl = min(idx / KV, nt - 1), key = (idx % KV) / (D / 8), c = idx % (D / 8);
+      kreg[i] = ld16(krow(min(kr0 + tl * kBN + key, kend - 1)) + c * 8);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int idx = i * NT + t;  // (tile, 4-key group, 8-dim chunk)
-      if (idx < nt * VB) {
-        const int tl = idx / VB, kg = idx % 16, dc = (idx % VB) / 16;
+      const int tl = min(idx / VB, nt - 1), kg = idx % 16, dc = (idx % VB) / 16;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          vreg[i][j] = ld16(cvv + row_off(min(kr0 + tl * kBN + kg * 4 + j, kend - 1)) + dc * 8);
-      }
+      for (int j = 0; j < 4; ++j) vreg[i][j] = ld16(vrow(min(kr0 + tl * kBN + kg * 4 + j, kend - 1)) + dc * 8);
     }
     if (kr0 != k0) __syncthreads();  // the previous round's tiles are no longer read
 #pragma unroll
     for (int i = 0; i < KPT; ++i) {
       const int idx = i * NT + t;
-      if (idx < nt * KV) {
-        const int tl = idx / KV, key = (idx % KV) / (D / 8), c = idx % (D / 8);
-        st16(&tiles[tl].k[key * Tile::KROW + c * 8], kreg[i]);
-      }
+      const int tl = min(idx / KV, nt - 1), key = (idx % KV) / (D / 8), c = idx % (D / 8);
+      st16(&tiles[tl].k[key * Tile::KROW + c * 8], kreg[i]);
     }
 #pragma unroll
     for (int i = 0; i < VPT; ++i) {
       const int idx = i * NT + t;
-      if (idx < nt * VB) {
-        const int tl = idx / VB, kg = idx % 16, dc = (idx % VB) / 16;
-        // vreg[i][j] = V[key 4kg + j][dims 8dc .. +7]; transposed row e = V[4kg .. 4kg + 3][8dc + e]
-        const uint32_t* x = reinterpret_cast<const uint32_t*>(vreg[i]);
+      const int tl = min(idx / VB, nt - 1), kg = idx % 16, dc = (idx % VB) / 16;
+      // vreg[i][j] = V[key 4kg + j][dims 8dc .. +7]; transposed row e = V[4kg .. 4kg + 3][8dc + e]
+      const uint32_t* x = reinterpret_cast<const uint32_t*>(vreg[i]);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-          const uint32_t w01 = __builtin_amdgcn_perm(x[4 + e / 2], x[e / 2], sel);
-          const uint32_t w23 = __builtin_amdgcn_perm(x[12 + e / 2], x[8 + e / 2], sel);
-          *reinterpret_cast<uint2*>(&tiles[tl].vt[(dc * 8 + e) * Tile::VROW + kg * 4]) = make_uint2(w01, w23);
-        }
+      for (int e = 0; e < 8; ++e) {
+        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
+        const uint32_t w01 = __builtin_amdgcn_perm(x[4 + e / 2], x[e / 2], sel);
+        const uint32_t w23 = __builtin_amdgcn_perm(x[12 + e / 2], x[8 + e / 2], sel);
+        *reinterpret_cast<uint2*>(&tiles[tl].vt[(dc * 8 + e) * Tile::VROW + kg * 4]) = make_uint2(w01, w23);
       }
     }
     __syncthreads();
@@ -185,8 +198,24 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
           st[rt][kt] = c;
         }
       }
-      // mask only tiles that reach past a row's position or the split's end
-      const bool need_mask = kb + kBN > kend || kb + kBN - 1 > rb.rmin;
+      // causal / split-end mask, only on tiles that reach past the block's
+      // first query position or the split's end (a block-uniform branch)
+      if (kb + kBN > kend || kb + kBN - 1 > rb.rmin) {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+          // key kb + 16 kt + 4 lq + e is visible iff 16 kt + e <= lim.  The
+          // empty asm keeps the compiler from hoisting this out of the loop,
+          // which would wait for the metadata load before the first K/V load.
+          int rp = rpos[rt];
+          asm volatile("" : "+v"(rp));
+          rp = 32 * w + 16 * rt + lr < rows ? rp : -1;
+          const int lim = min(rp, kend - 1) - kb - 4 * lq;
+#pragma unroll
+          for (int kt = 0; kt < 4; ++kt)
+#pragma unroll
+            for (int e = 0; e < 4; ++e) st[rt][kt][e] = (16 * kt + e <= lim) ? st[rt][kt][e] : -INFINITY;
+        }
+      }
       uint4 pb[2][2];
 #pragma unroll
       for (int rt = 0; rt < 2; ++rt) {
@@ -194,15 +223,7 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            float sv = st[rt][kt][e];
-            if (need_mask) {
-              const int p = kb + kt * 16 + lq * 4 + e;
-              sv = (p <= rpos[rt] && p < kend) ? sv : -INFINITY;
-            }
-            st[rt][kt][e] = sv;
-            tmax = fmaxf(tmax, sv);
-          }
+          for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, st[rt][kt][e]);
         tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
         tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
         tmax *= qscale;  // scores are scaled inside the exponent below
@@ -264,8 +285,7 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
     if (r >= rows) continue;
     if (part < 0) {
       const float inv = l > 0.f ? 1.f / l : 0.f;
-      const int tok = meta[rb.rank0 + r / g].tok;
-      bf16_t* o = out + ((int64_t)tok * Hq + hk * g + r % g) * D + lq * 4;
+      bf16_t* o = out + ((int64_t)rtok[rt] * Hq + hk * g + r % g) * D + lq * 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 a = acc[rt][dt];
@@ -273,13 +293,16 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
             make_uint2(cvt_bf16x2(a[0] * inv, a[1] * inv), cvt_bf16x2(a[2] * inv, a[3] * inv));
       }
     } else {
-      // partial outputs in bf16 (the merge weights them in fp32; they end in bf16)
+      // partial outputs in bf16 (the merge weights them in fp32; they end in
+      // bf16), stored in accumulator order: per 16-row and 16-dim tile the 64
+      // lanes' 4 values, so every store covers 512 contiguous bytes
       const int64_t pr = ((int64_t)part * Hkv + hk) * part_stride_rows + r;
-      bf16_t* o = reinterpret_cast<bf16_t*>(part_o) + pr * D + lq * 4;
+      bf16_t* o = reinterpret_cast<bf16_t*>(part_o) + ((int64_t)part * Hkv + hk) * part_stride_rows * D +
+                  ((int64_t)(2 * w + rt) * DT * 64 + lane) * 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 a = acc[rt][dt];
-        *reinterpret_cast<uint2*>(o + dt * 16) = make_uint2(cvt_bf16x2(a[0], a[1]), cvt_bf16x2(a[2], a[3]));
+        *reinterpret_cast<uint2*>(o + dt * 256) = make_uint2(cvt_bf16x2(a[0], a[1]), cvt_bf16x2(a[2], a[3]));
       }
       if (lq == 0) {
         part_ml[pr * 2 + 0] = mrow[rt];
@@ -292,17 +315,20 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
                      int part_stride_rows, hipStream_t s) {
-  if (args.n_items == 0) return 0;
-  dim3 grid(args.n_items, cv.n_kv_heads);
-  const int waves = part_stride_rows / 32;  // rows per block / 32
-#define PF(DD, PG, WV)                                                                                      \
-  hipLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV>), grid, dim3(WV * 64), 0, s, args, meta,         \
+  if (args.n_rb == 0 || args.n_split == 0) return 0;
+  dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
+  const int waves = part_stride_rows / 32;      // rows per block / 32
+  const bool stage4 = args.span > 2 * kBN;      // splits of more than two tiles stage four per round
+#define PF(DD, PG, WV, ST)                                                                                  \
+  hipLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, ST>), grid, dim3(WV * 64), 0, s, args, meta,     \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFW(DD, PG) { if (waves == 8) PF(DD, PG, 8); else PF(DD, PG, 4); }
+#define PFS(DD, PG, WV) { if (stage4) PF(DD, PG, WV, 4); else PF(DD, PG, WV, 2); }
+#define PFW(DD, PG) { if (waves == 8) PFS(DD, PG, 8) else PFS(DD, PG, 4) }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
   else { if (paged) PFW(64, true) else PFW(64, false) }
 #undef PFW
+#undef PFS
 #undef PF
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;

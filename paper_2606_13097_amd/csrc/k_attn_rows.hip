@@ -164,13 +164,13 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
 constexpr int kCombRows = 8;
 constexpr int kCombMaxParts = 256;
 
-template <typename T, int D, bool PART_BF16>
+template <typename T, int D, bool MFMA_PART>
 __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restrict__ items,
                                                       const TokenMeta* __restrict__ meta, int Hq, int Hkv,
                                                       const float* __restrict__ part_o,
                                                       const float* __restrict__ part_ml, int part_stride_rows,
                                                       T* __restrict__ out) {
-  __shared__ float s_f[kCombRows][kCombMaxParts];
+  __shared__ float s_f[kCombRows][kCombMaxParts + 1];  // +1: rows start in different banks
   __shared__ float4 s_acc[256];
   const CombineItem it = items[blockIdx.x];
   const int hk = blockIdx.y;
@@ -203,16 +203,29 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restr
   constexpr int CPR = D / 4;                  // 4-dim chunks per row
   const int nch = nr * CPR;
   const int lpc = max(1, 256 / nch);          // lanes per chunk (power of two: nr, CPR are)
+  // chunk c -> (row, 4-dim chunk): neighbouring lanes read neighbouring bytes
+  // (rows fastest in the MFMA fragment order, dims fastest in row-major order)
+  auto chunk = [&](int c, int* r, int* c4) {
+    *r = MFMA_PART ? c % nr : c / CPR;
+    *c4 = MFMA_PART ? c / nr : c % CPR;
+  };
   for (int c = t / lpc; c < nch; c += 256 / lpc) {
     const int sub = t % lpc;
-    const int r = c / CPR, c4 = c % CPR;
+    int r, c4;
+    chunk(c, &r, &c4);
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll 8
     for (int s = sub; s < np; s += lpc) {
       const float f = s_f[r][s];
       float4 o;
-      if (PART_BF16) {
-        const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const bf16_t*>(part_o) + prow(s, r) * D + c4 * 4);
+      if (MFMA_PART) {
+        // bf16, in the MFMA accumulator order of the prefill kernel: per
+        // 16-row tile and 16-dim tile, 64 lanes x 4 dims, lane = row % 16 +
+        // 16 * (4-dim chunk % 4)
+        const int rr = r0 + r;
+        const int64_t off = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows * D +
+                            (((rr / 16) * (D / 16) + c4 / 4) * 64 + rr % 16 + 16 * (c4 % 4)) * 4;
+        const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const bf16_t*>(part_o) + off);
         o = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
       } else {
         o = *reinterpret_cast<const float4*>(part_o + prow(s, r) * D + c4 * 4);
@@ -244,7 +257,8 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restr
       acc.z += a4.z;
       acc.w += a4.w;
     }
-    const int r = t / CPR, c4 = t % CPR;
+    int r, c4;
+    chunk(t, &r, &c4);
     const TokenMeta m = meta[it.rank0 + (r0 + r) / g];
     T* dst = out + ((int64_t)m.tok * Hq + hk * g + (r0 + r) % g) * D + c4 * 4;
     Store<T>::store1(dst + 0, acc.x);
@@ -282,11 +296,11 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq, int Hkv,
                    int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool part_bf16) {
+                   hipStream_t s, bool mfma_part) {
   if (n_items == 0) return 0;
   dim3 grid(n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
 #define CB(T, DD)                                                                                            \
-  if (part_bf16)                                                                                             \
+  if (mfma_part)                                                                                             \
     hipLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o,   \
                        part_ml, part_stride_rows, (T*)out);                                                  \
   else                                                                                                       \

@@ -1,25 +1,31 @@
-// One decode step at one layer for a batch of sequences, in a single launch
-// (Sec. 4.2, Eq. 6: decoding over the reused, grafted KV states).
+// One decode step at one layer for a batch of sequences (Sec. 4.2, Eq. 6:
+// decoding over the reused, grafted KV states).
 //
 // Per sequence i the new token sits at position pos_i = its current length.
-// Block (split s of sequence i, kv head h) attends the token's g query heads
+// Block (split s, sequence i, kv head h) attends the token's g query heads
 // over key positions [s * split_keys, min(pos_i + 1, (s + 1) * split_keys)):
-//   - it encodes the token's queries at pos_i (cos/sin of the position in
-//     LDS, fp64 angle), rounds them to storage and pre-scales them by
-//     log2(e) / sqrt(D) for a base-2 softmax;
+//   - before anything else it issues the loads of its first chunk of cached
+//     keys and values, of the query rows, of the new token's key and value
+//     and of the rotary frequencies, so the block pays one memory latency
+//     before its first math; every load is unconditional (positions past the
+//     range re-read its last key, scores masked), which keeps the compiler's
+//     load counting exact;
+//   - it encodes the queries at pos_i (cos/sin of the position in LDS, fp64
+//     angle), rounds them to storage and pre-scales them by log2(e) / sqrt(D)
+//     for a base-2 softmax;
+//   - cached keys stream through 16-byte vector loads, LPK lanes per key, U
+//     key steps per chunk, the next chunk in flight while one is reduced;
+//     scores are summed across a key's lanes with DPP, and each lane keeps an
+//     online softmax rescaled once per chunk;
 //   - the block whose split holds pos_i also encodes the new key, stores key
 //     and value into the cache slot and attends to them from registers; no
 //     other block touches that slot;
-//   - cached keys stream through 16-byte vector loads, LPK lanes per key,
-//     U key steps (U * 256 / LPK keys) in flight per lane before any math;
-//     scores are reduced across a key's lanes with DPP, and each lane keeps
-//     an online softmax rescaled once per chunk of U steps;
 //   - the block merges its key slots through LDS; a single-split sequence
 //     writes its output, otherwise the block stores a partial (max, sum,
-//     unnormalised output) that the combine kernel merges.  The merge is a
-//     separate launch on purpose: merging in the last-arriving block needs a
-//     device-scope release/acquire per block, which on gfx950 writes back
-//     and invalidates the XCD's whole L2.
+//     unnormalised output) that the decode merge kernel combines.  The merge
+//     is a separate launch on purpose: merging in the last-arriving block
+//     needs a device-scope release/acquire per block, which on gfx950 writes
+//     back and invalidates the XCD's whole L2.
 #include "fcg_device.hpp"
 #include "kernels.hpp"
 
@@ -39,30 +45,6 @@ __device__ __forceinline__ float lanes_sum(float x) {
   return x;
 }
 
-// Lane's rotated dims [d0, d0 + DPL) of a row x (storage T), encoded with the
-// block's cos/sin table; rounded to storage and returned as fp32.
-template <typename T, int D, int DPL>
-__device__ __forceinline__ void encode_dims(const T* __restrict__ x, int d0, const float* s_cos, const float* s_sin,
-                                            float* y) {
-  constexpr int VEC = Store<T>::VEC;
-  constexpr int HALF = D / 2;
-  float a[DPL], b[DPL];
-  const int dp = d0 < HALF ? d0 + HALF : d0 - HALF;  // partner dims
-#pragma unroll
-  for (int nv = 0; nv < DPL / VEC; ++nv) {
-    Store<T>::unpack(ld16(x + d0 + nv * VEC), a + nv * VEC);
-    Store<T>::unpack(ld16(x + dp + nv * VEC), b + nv * VEC);
-  }
-#pragma unroll
-  for (int e = 0; e < DPL; ++e) {
-    const int i = (d0 + e) % HALF;
-    const float c = s_cos[i], s = s_sin[i];
-    // first half: x_i c - x_{i+D/2} s; second half: x_{i+D/2} c + x_i s
-    const float r = d0 < HALF ? fmaf(a[e], c, -b[e] * s) : fmaf(a[e], c, b[e] * s);
-    y[e] = Store<T>::round(r);
-  }
-}
-
 template <typename T, int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* __restrict__ q,
                                                      const T* __restrict__ k, const T* __restrict__ v, CacheView cv,
@@ -71,41 +53,104 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
                                                      float* __restrict__ part_ml) {
   constexpr int VEC = Store<T>::VEC;
   constexpr int NV = (D / VEC > 16) ? (D / VEC) / 16 : 1;
-  constexpr int DPL = VEC * NV;
-  constexpr int LPK = D / DPL;
-  constexpr int SLOTS = 256 / LPK;
-  constexpr int U = G >= 8 ? 4 : 8;
+  constexpr int DPL = VEC * NV;    // dims per lane
+  constexpr int LPK = D / DPL;     // lanes per key
+  constexpr int SLOTS = 256 / LPK; // keys per step
+  constexpr int U = G >= 8 ? 2 : 4;  // steps per chunk
+  constexpr int CK = U * SLOTS;    // keys per chunk
   constexpr int HALF = D / 2;
+  constexpr int JB = G < 4 ? G : 4;  // query heads per LDS merge round
   __shared__ float s_cos[HALF], s_sin[HALF];
   __shared__ float s_m[SLOTS][G], s_l[SLOTS][G];
-  __shared__ float s_o[SLOTS][DPL][LPK];
+  __shared__ float s_o[SLOTS][JB][D];
   __shared__ float s_M[G], s_L[G];
 
-  // which sequence and split this block serves
-  const int b = blockIdx.x;
-  int i = 0;
-  while (i + 1 < args.n && args.split0[i + 1] <= b) ++i;
-  const int split = b - args.split0[i];
-  const int nsplit = args.split0[i + 1] - args.split0[i];
-  const int seq = args.seq[i], pos = args.pos[i];
-  const int hk = blockIdx.y;
+  const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
+  const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
+  const int nsplit = args.split0[i + 1] - slot0;
+  const int sk = args.split_keys;
+  const T* ck = reinterpret_cast<const T*>(cv.k);
+  const T* cvv = reinterpret_cast<const T*>(cv.v);
+  // every kernel argument in one batch of scalar loads before the first branch
+  asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
+               "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
+               "s"(out), "s"(part_o), "s"(part_ml));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
+  if (split >= nsplit) return;  // padding split of a shorter sequence
+
   const int Hkv = cv.n_kv_heads;
   const int Hq = Hkv * G;
   const int t = threadIdx.x;
   const int chunk = t % LPK, slot = t / LPK;
   const int d0 = chunk * DPL;
-  const int k0 = split * args.split_keys;
-  const int k1 = min(pos + 1, k0 + args.split_keys);
-  const bool owns_new = k0 <= pos && pos < k1;
+  const int dp = d0 < HALF ? d0 + HALF : d0 - HALF;  // rotary partner dims
+  const int k0 = split * sk;
+  const int k1 = min(pos + 1, k0 + sk);
+  const bool owns_new = k1 == pos + 1;  // the last split holds the new token
+  const int kend = owns_new ? pos : k1;  // cached keys [k0, kend)
 
+  auto load_chunk = [&](int b, uint4 (&kk)[U][NV], uint4 (&vv)[U][NV]) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int p = max(0, min(b + u * SLOTS + slot, kend - 1));
+      const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, p) + d0;
+#pragma unroll
+      for (int nv = 0; nv < NV; ++nv) {
+        kk[u][nv] = ld16(ck + off + nv * VEC);
+        vv[u][nv] = ld16(cvv + off + nv * VEC);
+      }
+    }
+  };
+  // two chunks in flight from the start (a chunk past the range re-reads its
+  // last key: one row, cached)
+  uint4 kr0[U][NV], vr0[U][NV], kr1[U][NV], vr1[U][NV];
+  load_chunk(k0, kr0, vr0);
+  load_chunk(k0 + CK, kr1, vr1);
+  // raw query rows, new key (dims and partner dims) and new value
+  uint4 qa[G][NV], qb[G][NV], na[NV], nb[NV], nvv[NV];
+#pragma unroll
+  for (int j = 0; j < G; ++j)
+#pragma unroll
+    for (int nv = 0; nv < NV; ++nv) {
+      const T* row = q + ((int64_t)i * Hq + hk * G + j) * D;
+      qa[j][nv] = ld16(row + d0 + nv * VEC);
+      qb[j][nv] = ld16(row + dp + nv * VEC);
+    }
+  {
+    const T* krow = k + ((int64_t)i * Hkv + hk) * D;
+    const T* vrow = v + ((int64_t)i * Hkv + hk) * D;
+#pragma unroll
+    for (int nv = 0; nv < NV; ++nv) {
+      na[nv] = ld16(krow + d0 + nv * VEC);
+      nb[nv] = ld16(krow + dp + nv * VEC);
+      nvv[nv] = ld16(vrow + d0 + nv * VEC);
+    }
+  }
   if (t < HALF) rope_cs((double)pos, inv_freq[t], &s_cos[t], &s_sin[t]);
   __syncthreads();
 
+  // rotate lane dims [d0, d0 + DPL) of a row given as (own dims, partner dims)
+  auto encode = [&](const uint4 (&xa)[NV], const uint4 (&xb)[NV], float* y) {
+    float a[DPL], bb[DPL];
+#pragma unroll
+    for (int nv = 0; nv < NV; ++nv) {
+      Store<T>::unpack(xa[nv], a + nv * VEC);
+      Store<T>::unpack(xb[nv], bb + nv * VEC);
+    }
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) {
+      const int ii = (d0 + e) % HALF;
+      const float c = s_cos[ii], sn = s_sin[ii];
+      // first half: x_i c - x_{i+D/2} s; second half: x_{i+D/2} c + x_i s
+      const float r = d0 < HALF ? fmaf(a[e], c, -bb[e] * sn) : fmaf(a[e], c, bb[e] * sn);
+      y[e] = Store<T>::round(r);
+    }
+  };
   const float qscale = 1.4426950408889634f / sqrtf((float)D);
   float qf[G][DPL];
 #pragma unroll
   for (int j = 0; j < G; ++j) {
-    encode_dims<T, D, DPL>(q + ((int64_t)i * Hq + hk * G + j) * D, d0, s_cos, s_sin, qf[j]);
+    encode(qa[j], qb[j], qf[j]);
 #pragma unroll
     for (int e = 0; e < DPL; ++e) qf[j][e] *= qscale;
   }
@@ -119,39 +164,24 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     for (int e = 0; e < DPL; ++e) o[j][e] = 0.f;
   }
 
-  const T* ck = reinterpret_cast<const T*>(cv.k);
-  const T* cvv = reinterpret_cast<const T*>(cv.v);
-  const int kend = owns_new ? pos : k1;  // cached keys; the new one is handled below
-  for (int base = k0; base < kend; base += U * SLOTS) {
-    // raw 16-byte vectors, all U steps in flight before any math; keys past
-    // the split re-read its last cached key (valid, scores masked)
-    uint4 kr[U][NV], vr[U][NV];
-    bool ok[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int key = base + u * SLOTS + slot;
-      ok[u] = key < kend;
-      const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, min(key, kend - 1)) + d0;
-#pragma unroll
-      for (int nv = 0; nv < NV; ++nv) {
-        kr[u][nv] = ld16(ck + off + nv * VEC);
-        vr[u][nv] = ld16(cvv + off + nv * VEC);
-      }
-    }
+  // online softmax over one chunk of keys [b, b + CK) held in registers
+  auto reduce_chunk = [&](int b, const uint4 (&kk)[U][NV], const uint4 (&vv)[U][NV]) {
     float s[U][G];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int u = 0; u < U; ++u) {
+      const bool ok = b + u * SLOTS + slot < kend;
+      float kx[DPL];
+#pragma unroll
+      for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(kk[u][nv], kx + nv * VEC);
 #pragma unroll
       for (int j = 0; j < G; ++j) {
-        float kx[DPL];
-#pragma unroll
-        for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(kr[u][nv], kx + nv * VEC);
         float a = 0.f;
 #pragma unroll
         for (int e = 0; e < DPL; ++e) a = fmaf(qf[j][e], kx[e], a);
         a = lanes_sum<LPK>(a);
-        s[u][j] = ok[u] ? a : -INFINITY;
+        s[u][j] = ok ? a : -INFINITY;
       }
+    }
 #pragma unroll
     for (int j = 0; j < G; ++j) {
       float cm = s[0][j];
@@ -169,26 +199,36 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
         acc_l += p;
         float vx[DPL];
 #pragma unroll
-        for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(vr[u][nv], vx + nv * VEC);
+        for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(vv[u][nv], vx + nv * VEC);
 #pragma unroll
         for (int e = 0; e < DPL; ++e) o[j][e] = fmaf(p, vx[e], o[j][e]);
       }
       sm[j] = acc_l;
       mx[j] = mn;
     }
+  };
+  // two register sets: the chunk after next is in flight while one is reduced
+  for (int b = k0; b < kend; b += 2 * CK) {
+    reduce_chunk(b, kr0, vr0);
+    if (b + CK >= kend) break;
+    load_chunk(b + 2 * CK, kr0, vr0);
+    reduce_chunk(b + CK, kr1, vr1);
+    load_chunk(b + 3 * CK, kr1, vr1);
   }
+
   if (owns_new && slot == 0) {
     // encode, store and attend the new token (lanes of slot 0)
     float kn[DPL], vn[DPL];
-    encode_dims<T, D, DPL>(k + ((int64_t)i * Hkv + hk) * D, d0, s_cos, s_sin, kn);
+    encode(na, nb, kn);
 #pragma unroll
-    for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(ld16(v + ((int64_t)i * Hkv + hk) * D + d0 + nv * VEC), vn + nv * VEC);
-    T* kdst = reinterpret_cast<T*>(cv.k) + kv_offset<PAGED>(cv, layer, seq, hk, pos) + d0;
-    T* vdst = reinterpret_cast<T*>(cv.v) + kv_offset<PAGED>(cv, layer, seq, hk, pos) + d0;
+    for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(nvv[nv], vn + nv * VEC);
+    const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, pos) + d0;
+    T* kdst = reinterpret_cast<T*>(cv.k) + off;
+    T* vdst = reinterpret_cast<T*>(cv.v) + off;
 #pragma unroll
     for (int nv = 0; nv < NV; ++nv) {
       st16(kdst + nv * VEC, Store<T>::pack(kn + nv * VEC));
-      st16(vdst + nv * VEC, Store<T>::pack(vn + nv * VEC));
+      st16(vdst + nv * VEC, nvv[nv]);
     }
 #pragma unroll
     for (int j = 0; j < G; ++j) {
@@ -222,26 +262,31 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     s_L[t] = L;
   }
   __syncthreads();
-  // partial slot of this split in the combine layout [slot][Hkv][G][D] (+ [slot][Hkv][G][2])
-  const int64_t prow = ((int64_t)(args.split0[i] + split) * Hkv + hk) * G;
+  // partial slot of this split in the merge layout [slot][Hkv][G][D] (+ [slot][Hkv][G][2])
+  const int64_t prow = ((int64_t)(slot0 + split) * Hkv + hk) * G;
 #pragma unroll
-  for (int j = 0; j < G; ++j) {
-    const float M = s_M[j];
-    const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : exp2f(mx[j] - M);
+  for (int jb = 0; jb < G; jb += JB) {
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) s_o[slot][e][chunk] = o[j][e] * f;
+    for (int jj = 0; jj < JB; ++jj) {
+      const int j = jb + jj;
+      const float M = s_M[j];
+      const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : exp2f(mx[j] - M);
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) s_o[slot][jj][d0 + e] = o[j][e] * f;
+    }
     __syncthreads();
-    for (int d = t; d < D; d += 256) {
-      const int c = d / DPL, e = d % DPL;
+    for (int idx = t; idx < JB * D; idx += 256) {
+      const int jj = idx / D, d = idx % D, j = jb + jj;
       float acc = 0.f;
-      for (int s2 = 0; s2 < SLOTS; ++s2) acc += s_o[s2][e][c];
+#pragma unroll 8
+      for (int s2 = 0; s2 < SLOTS; ++s2) acc += s_o[s2][jj][d];
       if (nsplit == 1) {
         const float L = s_L[j];
         Store<T>::store1(out + ((int64_t)i * Hq + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
       } else {
         part_o[(prow + j) * D + d] = acc;
         if (d == 0) {
-          part_ml[(prow + j) * 2 + 0] = M;
+          part_ml[(prow + j) * 2 + 0] = s_M[j];
           part_ml[(prow + j) * 2 + 1] = s_L[j];
         }
       }
@@ -250,12 +295,56 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   }
 }
 
+// Merge of the decode partials: block (sequence, kv head, query head of the
+// group), one lane per output dim.  O = sum_s O_s 2^(M_s - M) / sum_s L_s
+// 2^(M_s - M) with M = max_s M_s.  The first 32 splits' partial rows are
+// loaded together with the (M_s, L_s) pairs.
+template <typename T, int D, int G>
+__global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, const float* __restrict__ part_o,
+                                                           const float* __restrict__ part_ml, int Hkv,
+                                                           T* __restrict__ out) {
+  constexpr int P0 = 32;
+  __shared__ float s_m[256], s_l[256];
+  const int i = blockIdx.x, hk = blockIdx.y, j = blockIdx.z;
+  const int slot0 = args.split0[i];
+  const int ns = args.split0[i + 1] - slot0;
+  asm volatile("" ::"s"(slot0), "s"(ns), "s"(part_o), "s"(part_ml), "s"(out), "s"(Hkv));
+  if (ns <= 1) return;  // written by the decode kernel
+  const int d = threadIdx.x;
+  auto row = [&](int s) { return ((int64_t)(slot0 + s) * Hkv + hk) * G + j; };
+  float ov[P0];
+#pragma unroll
+  for (int u = 0; u < P0; ++u) ov[u] = part_o[row(min(u, ns - 1)) * D + d];
+  for (int s = d; s < ns; s += D) {
+    s_m[s] = part_ml[row(s) * 2 + 0];
+    s_l[s] = part_ml[row(s) * 2 + 1];
+  }
+  __syncthreads();
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, s_m[s]);
+  float L = 0.f, acc = 0.f;
+#pragma unroll
+  for (int u = 0; u < P0; ++u) {
+    const float m = s_m[min(u, ns - 1)];
+    const float w = (u < ns && m != -INFINITY) ? exp2f(m - M) : 0.f;
+    L = fmaf(s_l[min(u, ns - 1)], w, L);
+    acc = fmaf(ov[u], w, acc);
+  }
+  for (int s = P0; s < ns; ++s) {
+    const float m = s_m[s];
+    const float w = m != -INFINITY ? exp2f(m - M) : 0.f;
+    L = fmaf(s_l[s], w, L);
+    acc = fmaf(part_o[row(s) * D + d], w, acc);
+  }
+  Store<T>::store1(out + ((int64_t)i * Hkv * G + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
+}
+
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
                   hipStream_t s) {
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
-  dim3 grid(args.split0[args.n], cv.n_kv_heads);
+  dim3 grid(args.max_split, args.n, cv.n_kv_heads);
 #define DK(T, DD, GG)                                                                                       \
   if (cv.page_size)                                                                                         \
     hipLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, args, (const T*)q,          \
@@ -276,6 +365,30 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
   else { if (cv.head_dim == 64) { DKG(bf16_t, 64) } else { DKG(bf16_t, 128) } }
 #undef DKG
 #undef DK
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : (int)e;
+}
+
+int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
+                          const float* part_ml, void* out, hipStream_t s) {
+  if (args.n == 0 || args.max_split <= 1) return 0;
+  const int g = Hq / Hkv;
+  dim3 grid(args.n, Hkv, g);
+#define DC(T, DD, GG)                                                                                       \
+  hipLaunchKernelGGL((decode_combine_kernel<T, DD, GG>), grid, dim3(DD), 0, s, args, part_o, part_ml, Hkv, (T*)out)
+#define DCG(T, DD)                                                                                          \
+  switch (g) {                                                                                              \
+    case 1: DC(T, DD, 1); break;                                                                            \
+    case 2: DC(T, DD, 2); break;                                                                            \
+    case 4: DC(T, DD, 4); break;                                                                            \
+    case 8: DC(T, DD, 8); break;                                                                            \
+    case 16: DC(T, DD, 16); break;                                                                          \
+    default: return -1;                                                                                     \
+  }
+  if (dtype == 0) { if (D == 64) { DCG(float, 64) } else { DCG(float, 128) } }
+  else { if (D == 64) { DCG(bf16_t, 64) } else { DCG(bf16_t, 128) } }
+#undef DCG
+#undef DC
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

@@ -78,10 +78,11 @@ constexpr int kMaxDecodeSeqs = 64;
 struct DecodeArgs {
   int32_t n;           // sequences in this launch
   int32_t split_keys;  // key positions per split
-  int32_t pad0, pad1;
+  int32_t max_split;   // largest split count of the launch (grid x)
+  int32_t pad;
   int32_t seq[kMaxDecodeSeqs];
   int32_t pos[kMaxDecodeSeqs];         // the new token's position (= the sequence's length)
-  int32_t split0[kMaxDecodeSeqs + 1];  // first block of each sequence; split0[n] = grid size
+  int32_t split0[kMaxDecodeSeqs + 1];  // first partial slot of each sequence; split0[i + 1] - split0[i] splits
 };
 
 int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len,
@@ -96,20 +97,20 @@ int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, c
                        const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws,
                        hipStream_t s);
 
-// By-value work list of one MFMA prefill launch: row blocks (up to 128 query
-// rows of one sequence) and items (row block, key split of `span` positions),
-// so a block's first loads need no metadata round trip.
-constexpr int kPfMaxRb = 48;
-constexpr int kPfMaxItems = 512;
+// By-value work list of one MFMA prefill launch: row blocks (up to 256 query
+// rows of one sequence), each attended over n_split key splits of `span`
+// positions (splits past a row block's last position are empty).  The grid is
+// (row block, split, kv head), so a block finds its work without a memory
+// round trip.
+constexpr int kPfMaxRb = 128;
 struct PrefillRb {
   int32_t rank0, n_rank, seq;
   int32_t rmin, pmax;  // smallest and largest query position of the block
   int32_t part0;       // first partial slot, -1 when the block has a single split
 };
 struct PrefillArgs {
-  int32_t n_rb, n_items, span, pad;
+  int32_t n_rb, n_split, span, pad;
   PrefillRb rb[kPfMaxRb];
-  uint32_t item[kPfMaxItems];  // row block | split << 8
 };
 
 // bf16 MFMA attention of query-workspace rows over the cache.
@@ -123,16 +124,22 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
                      float* part_ml, int part_stride_rows, hipStream_t s);
 
 // Decode step: encode + store the new token and split-KV attention over the
-// cache.  q, k, v, out: [n][H][D] rows in the order of args.seq.  Splits of
-// multi-split sequences leave partials in part_o [slot][Hkv][g][D] and
-// part_ml [slot][Hkv][g][2], slot = split0[i] + split, for launch_combine.
+// cache.  q, k, v, out: [n][H][D] rows in the order of args.seq.  Grid
+// (max_split, n, Hkv).  Splits of multi-split sequences leave partials in
+// part_o [slot][Hkv][g][D] and part_ml [slot][Hkv][g][2], slot = split0[i] +
+// split, merged by launch_decode_combine.
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
                   hipStream_t s);
 
-// Merge split partials (part_o fp32, or bf16 when part_bf16) into out.
+// Merge the decode partials of the multi-split sequences of args into out.
+int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
+                          const float* part_ml, void* out, hipStream_t s);
+
+// Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
+// accumulator order of the MFMA prefill kernel.
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
                    int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool part_bf16 = false);
+                   hipStream_t s, bool mfma_part = false);
 
 }  // namespace fcg
