@@ -686,8 +686,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
 // One decode launch per group of up to kMaxDecodeSeqs sequences, then one
 // merge launch for the sequences split over several blocks; both take their
 // plan by value, so a decode step uploads nothing (new pages aside).  Split
-// size: enough blocks to cover the chip twice over, at least 128 keys per
-// block.
+// size: blocks fill the chip twice over in one wave.
 fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
                       const void* q, const void* k, const void* v, void* out,
                       const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
@@ -699,10 +698,18 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     total += pos[i] + 1;
     pmax = std::max(pmax, pos[i]);
   }
+  // split length: the smallest (from 64 keys up) whose blocks fit two per
+  // compute unit, so the grid runs in one wave; at most 256 splits per
+  // sequence (the merge table)
   const int64_t target_blocks = 512;
-  int64_t sk = (total * d.n_kv_heads + target_blocks - 1) / target_blocks;
-  sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);  // at most 256 splits per sequence (combine table)
-  sk = std::max<int64_t>(128, (sk + 127) / 128 * 128);
+  int64_t sk = std::max<int64_t>(64, (total * d.n_kv_heads + target_blocks - 1) / target_blocks);
+  sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);
+  for (;;) {
+    int64_t blocks = 0;
+    for (int32_t i = 0; i < n; ++i) blocks += (pos[i] + sk) / sk;
+    if (blocks * d.n_kv_heads <= target_blocks || blocks <= n) break;
+    sk += (sk + 31) / 32;  // about 3% longer
+  }
   // partial slots: one per split of every multi-split sequence of a launch group
   int max_slots = 0;
   for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {

@@ -36,6 +36,13 @@ __device__ __forceinline__ float dpp_f(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// a.lo * b.lo + a.hi * b.hi + c over bf16 pairs (v_dot2c_f32_bf16, fp32 accumulate)
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), c, false);
+}
+
 template <int LPK>
 __device__ __forceinline__ float lanes_sum(float x) {
   if (LPK >= 2) x += dpp_f<0xB1>(x);   // quad_perm [1,0,3,2]
@@ -60,10 +67,12 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   constexpr int CK = U * SLOTS;    // keys per chunk
   constexpr int HALF = D / 2;
   constexpr int JB = G < 4 ? G : 4;  // query heads per LDS merge round
+  constexpr bool BF = sizeof(T) == 2;  // bf16: scores with v_dot2 on packed pairs
+  constexpr int NW = DPL / 2;          // packed pairs per lane
   __shared__ float s_cos[HALF], s_sin[HALF];
   __shared__ float s_m[SLOTS][G], s_l[SLOTS][G];
   __shared__ float s_o[SLOTS][JB][D];
-  __shared__ float s_M[G], s_L[G];
+  __shared__ float s_L[G];
 
   const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
   const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
@@ -101,12 +110,11 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       }
     }
   };
-  // two chunks in flight from the start (a chunk past the range re-reads its
-  // last key: one row, cached)
-  uint4 kr0[U][NV], vr0[U][NV], kr1[U][NV], vr1[U][NV];
-  load_chunk(k0, kr0, vr0);
-  load_chunk(k0 + CK, kr1, vr1);
-  // raw query rows, new key (dims and partner dims) and new value
+  // loads in the order their data is needed (they complete in issue order):
+  // rotary frequency, raw query rows, new key (dims and partner dims) and
+  // value, then two chunks of cached keys (a chunk past the range re-reads
+  // its last key: one row, cached)
+  const double wfreq = inv_freq[t % HALF];
   uint4 qa[G][NV], qb[G][NV], na[NV], nb[NV], nvv[NV];
 #pragma unroll
   for (int j = 0; j < G; ++j)
@@ -126,7 +134,10 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       nvv[nv] = ld16(vrow + d0 + nv * VEC);
     }
   }
-  if (t < HALF) rope_cs((double)pos, inv_freq[t], &s_cos[t], &s_sin[t]);
+  uint4 kr0[U][NV], vr0[U][NV], kr1[U][NV], vr1[U][NV];
+  load_chunk(k0, kr0, vr0);
+  load_chunk(k0 + CK, kr1, vr1);
+  if (t < HALF) rope_cs((double)pos, wfreq, &s_cos[t], &s_sin[t]);
   __syncthreads();
 
   // rotate lane dims [d0, d0 + DPL) of a row given as (own dims, partner dims)
@@ -147,13 +158,37 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     }
   };
   const float qscale = 1.4426950408889634f / sqrtf((float)D);
+  // encoded queries: fp32 pre-scaled (fp32 storage), or the rounded bf16
+  // values packed in pairs, the score scaled after the dot product
   float qf[G][DPL];
+  uint32_t qp[G][NW];
 #pragma unroll
   for (int j = 0; j < G; ++j) {
     encode(qa[j], qb[j], qf[j]);
 #pragma unroll
+    for (int e = 0; e < NW; ++e)
+      qp[j][e] = (__float_as_uint(qf[j][2 * e]) >> 16) | (__float_as_uint(qf[j][2 * e + 1]) & 0xFFFF0000u);
+#pragma unroll
     for (int e = 0; e < DPL; ++e) qf[j][e] *= qscale;
   }
+  // scaled score of query head j against this lane's dims of a key
+  auto score = [&](int j, const uint4 (&kw)[NV], const float* kx) -> float {
+    float a = 0.f;
+    if constexpr (BF) {
+#pragma unroll
+      for (int nv = 0; nv < NV; ++nv) {
+        a = dot2_bf16(qp[j][4 * nv + 0], kw[nv].x, a);
+        a = dot2_bf16(qp[j][4 * nv + 1], kw[nv].y, a);
+        a = dot2_bf16(qp[j][4 * nv + 2], kw[nv].z, a);
+        a = dot2_bf16(qp[j][4 * nv + 3], kw[nv].w, a);
+      }
+      return lanes_sum<LPK>(a) * qscale;
+    } else {
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) a = fmaf(qf[j][e], kx[e], a);
+      return lanes_sum<LPK>(a);
+    }
+  };
 
   float mx[G], sm[G], o[G][DPL];
 #pragma unroll
@@ -171,14 +206,13 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     for (int u = 0; u < U; ++u) {
       const bool ok = b + u * SLOTS + slot < kend;
       float kx[DPL];
+      if constexpr (!BF) {
 #pragma unroll
-      for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(kk[u][nv], kx + nv * VEC);
+        for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(kk[u][nv], kx + nv * VEC);
+      }
 #pragma unroll
       for (int j = 0; j < G; ++j) {
-        float a = 0.f;
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) a = fmaf(qf[j][e], kx[e], a);
-        a = lanes_sum<LPK>(a);
+        const float a = score(j, kk[u], kx);
         s[u][j] = ok ? a : -INFINITY;
       }
     }
@@ -189,13 +223,13 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       for (int u = 1; u < U; ++u) cm = fmaxf(cm, s[u][j]);
       const float mn = fmaxf(mx[j], cm);
       if (mn == -INFINITY) continue;  // nothing seen yet by this lane
-      const float a = exp2f(mx[j] - mn);
+      const float a = __builtin_amdgcn_exp2f(mx[j] - mn);  // v_exp_f32: -inf gives 0
       float acc_l = sm[j] * a;
 #pragma unroll
       for (int e = 0; e < DPL; ++e) o[j][e] *= a;
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const float p = exp2f(s[u][j] - mn);  // 0 for masked keys (their values are finite)
+        const float p = __builtin_amdgcn_exp2f(s[u][j] - mn);  // 0 for masked keys
         acc_l += p;
         float vx[DPL];
 #pragma unroll
@@ -230,14 +264,14 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       st16(kdst + nv * VEC, Store<T>::pack(kn + nv * VEC));
       st16(vdst + nv * VEC, nvv[nv]);
     }
+    uint4 knw[NV];  // the rounded key, packed again (exact: bf16 values)
+#pragma unroll
+    for (int nv = 0; nv < NV; ++nv) knw[nv] = Store<T>::pack(kn + nv * VEC);
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-      float a = 0.f;
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) a = fmaf(qf[j][e], kn[e], a);
-      a = lanes_sum<LPK>(a);
+      const float a = score(j, knw, kn);
       const float mn = fmaxf(mx[j], a);
-      const float f = exp2f(mx[j] - mn), p = exp2f(a - mn);
+      const float f = __builtin_amdgcn_exp2f(mx[j] - mn), p = __builtin_amdgcn_exp2f(a - mn);
       sm[j] = fmaf(sm[j], f, p);
 #pragma unroll
       for (int e = 0; e < DPL; ++e) o[j][e] = fmaf(o[j][e], f, p * vn[e]);
@@ -245,34 +279,39 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     }
   }
 
-  // merge the block's key slots
+  // merge the block's key slots: every lane finds each head's block max M
+  // from the slots' maxima, scales its output by 2^(m - M) into LDS, and the
+  // block sums the slots per output element
   if (chunk == 0) {
 #pragma unroll
     for (int j = 0; j < G; ++j) { s_m[slot][j] = mx[j]; s_l[slot][j] = sm[j]; }
   }
   __syncthreads();
-  if (t < G) {
-    float M = -INFINITY;
-    for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][t]);
-    float L = 0.f;
-    if (M != -INFINITY)
-      for (int s2 = 0; s2 < SLOTS; ++s2)
-        if (s_m[s2][t] != -INFINITY) L += s_l[s2][t] * exp2f(s_m[s2][t] - M);
-    s_M[t] = M;
-    s_L[t] = L;
-  }
-  __syncthreads();
-  // partial slot of this split in the merge layout [slot][Hkv][G][D] (+ [slot][Hkv][G][2])
   const int64_t prow = ((int64_t)(slot0 + split) * Hkv + hk) * G;
 #pragma unroll
   for (int jb = 0; jb < G; jb += JB) {
+    if (jb) __syncthreads();  // the previous round's sums are read
 #pragma unroll
     for (int jj = 0; jj < JB; ++jj) {
       const int j = jb + jj;
-      const float M = s_M[j];
-      const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : exp2f(mx[j] - M);
+      float M = -INFINITY;
 #pragma unroll
-      for (int e = 0; e < DPL; ++e) s_o[slot][jj][d0 + e] = o[j][e] * f;
+      for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][j]);
+      const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mx[j] - M);
+#pragma unroll
+      for (int e = 0; e < DPL; e += 4)
+        *reinterpret_cast<float4*>(&s_o[slot][jj][d0 + e]) =
+            make_float4(o[j][e] * f, o[j][e + 1] * f, o[j][e + 2] * f, o[j][e + 3] * f);
+    }
+    if (jb == 0 && t < G) {  // block sums of the heads
+      float M = -INFINITY, L = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][t]);
+      if (M != -INFINITY) {
+#pragma unroll
+        for (int s2 = 0; s2 < SLOTS; ++s2) L = fmaf(s_l[s2][t], __builtin_amdgcn_exp2f(s_m[s2][t] - M), L);
+      }
+      s_L[t] = L;
     }
     __syncthreads();
     for (int idx = t; idx < JB * D; idx += 256) {
@@ -280,30 +319,33 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       float acc = 0.f;
 #pragma unroll 8
       for (int s2 = 0; s2 < SLOTS; ++s2) acc += s_o[s2][jj][d];
+      const float L = s_L[j];
       if (nsplit == 1) {
-        const float L = s_L[j];
         Store<T>::store1(out + ((int64_t)i * Hq + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
       } else {
+        // partial slot of this split in the merge layout [slot][Hkv][G][D] (+ [slot][Hkv][G][2])
         part_o[(prow + j) * D + d] = acc;
         if (d == 0) {
-          part_ml[(prow + j) * 2 + 0] = s_M[j];
-          part_ml[(prow + j) * 2 + 1] = s_L[j];
+          float M = -INFINITY;
+#pragma unroll
+          for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][j]);
+          part_ml[(prow + j) * 2 + 0] = M;
+          part_ml[(prow + j) * 2 + 1] = L;
         }
       }
     }
-    __syncthreads();
   }
 }
 
 // Merge of the decode partials: block (sequence, kv head, query head of the
 // group), one lane per output dim.  O = sum_s O_s 2^(M_s - M) / sum_s L_s
-// 2^(M_s - M) with M = max_s M_s.  The first 32 splits' partial rows are
+// 2^(M_s - M) with M = max_s M_s.  The first 64 splits' partial rows are
 // loaded together with the (M_s, L_s) pairs.
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, const float* __restrict__ part_o,
                                                            const float* __restrict__ part_ml, int Hkv,
                                                            T* __restrict__ out) {
-  constexpr int P0 = 32;
+  constexpr int P0 = 64;
   __shared__ float s_m[256], s_l[256];
   const int i = blockIdx.x, hk = blockIdx.y, j = blockIdx.z;
   const int slot0 = args.split0[i];
@@ -321,6 +363,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, cons
   }
   __syncthreads();
   float M = -INFINITY;
+#pragma unroll 8
   for (int s = 0; s < ns; ++s) M = fmaxf(M, s_m[s]);
   float L = 0.f, acc = 0.f;
 #pragma unroll
@@ -330,6 +373,7 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, cons
     L = fmaf(s_l[min(u, ns - 1)], w, L);
     acc = fmaf(ov[u], w, acc);
   }
+#pragma unroll 8
   for (int s = P0; s < ns; ++s) {
     const float m = s_m[s];
     const float w = m != -INFINITY ? exp2f(m - M) : 0.f;

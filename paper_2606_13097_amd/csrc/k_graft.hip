@@ -6,7 +6,9 @@
 // kernel is a pure HBM stream: each lane moves whole 16-byte vectors, the two
 // halves of a rotary pair are loaded by the same lane, all loads of a block are
 // issued before its stores, and data never passes through LDS (LDS holds only
-// the D/2 cos/sin values of the block's delta, computed once per block).
+// the D/2 cos/sin values of the block's delta, computed once per block).  The
+// library is read with the nontemporal hint (it is read once per graft); the
+// stores are plain, since the grafted cache is read next.
 //
 // ingest: copy a segment given token-major [L][len][Hkv][D] into the library's
 // head-major slabs [L][Hkv][cap][D].
@@ -71,14 +73,14 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
 #pragma unroll
   for (int p = 0; p < KP; ++p) {
     const int j = min(p * KR + kr, ch.n - 1);
-    klo[p] = ld16(sk + (int64_t)j * D + kc * VEC);
-    khi[p] = ld16(sk + (int64_t)j * D + HALF + kc * VEC);
+    klo[p] = ld16_nt(sk + (int64_t)j * D + kc * VEC);
+    khi[p] = ld16_nt(sk + (int64_t)j * D + HALF + kc * VEC);
   }
   const int vc = t % VT, vr = t / VT;
 #pragma unroll
   for (int p = 0; p < VP; ++p) {
     const int j = min(p * VR + vr, ch.n - 1);
-    vv[p] = ld16(sv + (int64_t)j * D + vc * VEC);
+    vv[p] = ld16_nt(sv + (int64_t)j * D + vc * VEC);
   }
   __syncthreads();  // cos/sin ready
 
