@@ -184,14 +184,17 @@ fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int
  *   FCG_TIME_PREFILL_ATTN the attention kernel of fcg_patch_prefill
  *   FCG_TIME_PREFILL      all kernels of fcg_patch_prefill (append, attention, merge)
  *   FCG_TIME_DECODE       all kernels of fcg_decode (attention, merge)
+ *   FCG_TIME_DECODE_ATTN  the attention kernel of fcg_decode
  * Plan uploads and host work are outside the intervals.  fcg_cache_timing_read
  * waits for the recorded events, returns the number of intervals and their
- * summed duration in milliseconds for one kind, and forgets them.  enable = 0
+ * summed duration in milliseconds for one kind (ERANGE for another value),
+ * and forgets them.  enable = 0
  * stops recording (recorded intervals stay readable). */
 #define FCG_TIME_GRAFT 0
 #define FCG_TIME_PREFILL_ATTN 1
 #define FCG_TIME_PREFILL 2
 #define FCG_TIME_DECODE 3
+#define FCG_TIME_DECODE_ATTN 4
 fcg_status fcg_cache_timing(fcg_cache* cache, int32_t enable);
 fcg_status fcg_cache_timing_read(fcg_cache* cache, int32_t kind, int32_t* count, double* total_ms);
 

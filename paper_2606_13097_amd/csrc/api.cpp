@@ -10,6 +10,7 @@
 #include <new>
 #include <string>
 #include <tuple>
+#include <unordered_map>
 #include <vector>
 
 #include "fcg.h"
@@ -183,8 +184,9 @@ struct fcg_cache {
   size_t dpart_bytes = 0;
   // kernel timing (fcg_cache_timing): recorded (start, end) event pairs per kind
   bool timing = false;
-  std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[4];
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[5];
   std::vector<hipEvent_t> ev_pool;
+  std::unordered_map<hipEvent_t, int> ev_refs;
 
   fcg_cache(const fcg_model_desc& d, int32_t ns, int32_t mt, int32_t ps, int32_t np, uint32_t fl)
       : desc(d), n_seqs(ns), max_tokens(mt), page_size(ps), n_pages(np), flags(fl),
@@ -209,32 +211,53 @@ struct fcg_cache {
 
 namespace {
 
+// Kernel timing.  Events come from a per-cache pool and are attached to
+// kernel dispatches (KTime); an event may close one interval and belong to
+// another (the last kernel of a call ends both its own interval and the
+// call's), so events carry a reference count and return to the pool at zero.
 hipEvent_t timing_event(fcg_cache* c) {
-  if (!c->ev_pool.empty()) {
-    hipEvent_t e = c->ev_pool.back();
-    c->ev_pool.pop_back();
-    return e;
-  }
+  if (!c->timing) return nullptr;
   hipEvent_t e = nullptr;
-  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  if (!c->ev_pool.empty()) {
+    e = c->ev_pool.back();
+    c->ev_pool.pop_back();
+  } else if (hipEventCreate(&e) != hipSuccess) {
+    return nullptr;
+  }
+  c->ev_refs[e] = 0;
   return e;
 }
 
-// Start an interval of `kind` on stream s (no-op unless timing is enabled).
-void time_begin(fcg_cache* c, int kind, hipStream_t s) {
-  if (!c->timing) return;
-  hipEvent_t a = timing_event(c);
-  if (!a) return;
-  hipEventRecord(a, s);
-  c->spans[kind].push_back({a, nullptr});
+void event_put(fcg_cache* c, hipEvent_t e) {
+  auto it = c->ev_refs.find(e);
+  if (it == c->ev_refs.end()) return;
+  if (--it->second <= 0) {
+    c->ev_refs.erase(it);
+    c->ev_pool.push_back(e);
+  }
 }
 
-void time_end(fcg_cache* c, int kind, hipStream_t s) {
-  if (!c->timing || c->spans[kind].empty() || c->spans[kind].back().second) return;
-  hipEvent_t b = timing_event(c);
-  if (!b) return;
-  hipEventRecord(b, s);
-  c->spans[kind].back().second = b;
+// Open an interval of `kind` at event e (the start event of a kernel).
+void time_open(fcg_cache* c, int kind, hipEvent_t e) {
+  if (!e) return;
+  ++c->ev_refs[e];
+  c->spans[kind].push_back({e, nullptr});
+}
+
+// Close the open interval of `kind` at event e (the stop event of a kernel).
+void time_close(fcg_cache* c, int kind, hipEvent_t e) {
+  if (!e || c->spans[kind].empty() || c->spans[kind].back().second) return;
+  ++c->ev_refs[e];
+  c->spans[kind].back().second = e;
+}
+
+// Unused events of a call (a kernel not launched) go back to the pool.
+void time_drop(fcg_cache* c, hipEvent_t e) {
+  auto it = c->ev_refs.find(e);
+  if (it != c->ev_refs.end() && it->second == 0) {
+    c->ev_refs.erase(it);
+    c->ev_pool.push_back(e);
+  }
 }
 
 fcg_status grow(void** p, size_t* have, size_t need, const char* what) {
@@ -472,7 +495,7 @@ fcg_status fcg_cache_timing(fcg_cache* c, int32_t enable) {
 
 fcg_status fcg_cache_timing_read(fcg_cache* c, int32_t kind, int32_t* count, double* total_ms) {
   if (!c) return fail(FCG_EINVAL, "null cache");
-  if (kind < 0 || kind > 3) return fail(FCG_ERANGE, "unknown timing kind");
+  if (kind < 0 || kind > FCG_TIME_DECODE_ATTN) return fail(FCG_ERANGE, "unknown timing kind");
   double ms = 0.0;
   int32_t n = 0;
   for (auto& sp : c->spans[kind]) {
@@ -482,9 +505,9 @@ fcg_status fcg_cache_timing_read(fcg_cache* c, int32_t kind, int32_t* count, dou
       HIP_TRY(hipEventElapsedTime(&t, sp.first, sp.second), "hipEventElapsedTime");
       ms += t;
       ++n;
-      c->ev_pool.push_back(sp.second);
+      event_put(c, sp.second);
     }
-    c->ev_pool.push_back(sp.first);
+    event_put(c, sp.first);
   }
   c->spans[kind].clear();
   if (count) *count = n;
@@ -557,10 +580,11 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   char* dev;
   size_t off;
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
-  time_begin(c, FCG_TIME_GRAFT, s);
+  const KTime tg{timing_event(c), timing_event(c)};
   int rc = launch_graft(c->desc.dtype, (const GraftChunk*)(dev + o_chunks), (int)chunks.size(), lib->k, lib->v,
-                        lib->cap, c->view(), c->d_inv_freq, c->desc.n_layers, s);
-  time_end(c, FCG_TIME_GRAFT, s);
+                        lib->cap, c->view(), c->d_inv_freq, c->desc.n_layers, s, tg);
+  time_open(c, FCG_TIME_GRAFT, tg.start);
+  time_close(c, FCG_TIME_GRAFT, tg.stop);
   if (rc) return hip_fail((hipError_t)rc, "graft launch");
   if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
   for (auto& sp : spans) c->plan.mark_all_layers(sp.seq, sp.dst, sp.len);
@@ -572,13 +596,13 @@ namespace {
 // Attention over the cache for tokens already sorted into TokenMeta ranks.
 // Builds the split plan, uploads it with the page rows, then runs
 // rope_append -> attention -> (combine).
-fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMeta>& meta, bool decode,
+fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMeta>& meta,
                          const void* q, const void* k, const void* v, void* out,
                          const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
   const fcg_model_desc& d = c->desc;
   const int n = (int)meta.size();
   const int g = d.n_q_heads / d.n_kv_heads;
-  const bool mfma = !decode && d.dtype == FCG_BF16;
+  const bool mfma = d.dtype == FCG_BF16;
   // row blocks: consecutive ranks of one sequence, at most 256 query rows (MFMA) or one token
   const int max_rank = mfma ? std::max(1, 256 / g) : 1;
   std::vector<std::pair<int, int>> rblocks;  // (rank0, n_rank)
@@ -657,29 +681,40 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
   const TokenMeta* dmeta = (const TokenMeta*)(dev + o_meta);
   const CacheView cv = c->view();
-  const int tk_all = decode ? FCG_TIME_DECODE : FCG_TIME_PREFILL;
-  time_begin(c, tk_all, s);
-  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_inv_freq, d.n_q_heads, c->qws, s);
+  // timing: the append kernel opens the call's interval, the attention
+  // launches bracket their own, the last kernel closes the call's
+  const hipEvent_t e_call0 = timing_event(c), e_attn0 = timing_event(c), e_attn1 = timing_event(c);
+  const hipEvent_t e_call1 = comb.empty() ? e_attn1 : timing_event(c);
+  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_inv_freq, d.n_q_heads, c->qws, s,
+                              KTime{e_call0, nullptr});
   if (rc) return hip_fail((hipError_t)rc, "append launch");
-  if (!decode) time_begin(c, FCG_TIME_PREFILL_ATTN, s);
   float* part_o = c->part;
   float* part_ml = c->part ? c->part + po : nullptr;
   if (mfma) {
-    for (const PrefillArgs& a : pf_launch) {
-      rc = launch_attn_mfma(a, dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
+    for (size_t li = 0; li < pf_launch.size(); ++li) {
+      const KTime tm{li == 0 ? e_attn0 : nullptr, li + 1 == pf_launch.size() ? e_attn1 : nullptr};
+      rc = launch_attn_mfma(pf_launch[li], dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml,
+                            stride_rows, s, tm);
       if (rc) break;
     }
   } else
     rc = launch_attn_rows(d.dtype, (const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv,
-                          layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s);
+                          layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s, KTime{e_attn0, e_attn1});
   if (rc) return hip_fail((hipError_t)rc, "attention launch");
-  if (!decode) time_end(c, FCG_TIME_PREFILL_ATTN, s);
   if (!comb.empty()) {
     rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), dmeta, d.n_q_heads,
-                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s, mfma);
+                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s, mfma, KTime{nullptr, e_call1});
     if (rc) return hip_fail((hipError_t)rc, "combine launch");
   }
-  time_end(c, tk_all, s);
+  if (mfma && pf_launch.empty()) {  // nothing attended: no attention interval
+    time_drop(c, e_attn0);
+    if (e_call1 != e_attn1) time_drop(c, e_attn1);
+  } else {
+    time_open(c, FCG_TIME_PREFILL_ATTN, e_attn0);
+    time_close(c, FCG_TIME_PREFILL_ATTN, e_attn1);
+  }
+  time_open(c, FCG_TIME_PREFILL, e_call0);
+  time_close(c, FCG_TIME_PREFILL, e_call1);
   return c->ring.retire(off, blob.bytes.size(), s);
 }
 
@@ -746,13 +781,23 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
       a.max_split = std::max(a.max_split, ns);
     }
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
-    time_begin(c, FCG_TIME_DECODE, s);
+    // timing: the decode kernel's dispatch opens both intervals and closes
+    // its own; the merge kernel (if launched) closes the call's
+    const bool merge = a.max_split > 1;
+    const hipEvent_t e0 = timing_event(c), e1 = timing_event(c);
+    const hipEvent_t e2 = merge ? timing_event(c) : e1;
     int rc = launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv, layer,
-                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, s);
+                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, s, KTime{e0, e1});
     if (rc) return hip_fail((hipError_t)rc, "decode launch");
-    rc = launch_decode_combine(d.dtype, a, d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml, (char*)out + qoff, s);
-    if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
-    time_end(c, FCG_TIME_DECODE, s);
+    if (merge) {
+      rc = launch_decode_combine(d.dtype, a, d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml,
+                                 (char*)out + qoff, s, KTime{nullptr, e2});
+      if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
+    }
+    time_open(c, FCG_TIME_DECODE_ATTN, e0);
+    time_close(c, FCG_TIME_DECODE_ATTN, e1);
+    time_open(c, FCG_TIME_DECODE, e0);
+    time_close(c, FCG_TIME_DECODE, e2);
   }
   return FCG_OK;
 }
@@ -780,7 +825,7 @@ fcg_status fcg_patch_prefill(fcg_cache* c, int32_t layer, int32_t n_tok, const i
   std::sort(meta.begin(), meta.end(), [](const TokenMeta& a, const TokenMeta& b) {
     return a.seq != b.seq ? a.seq < b.seq : a.pos < b.pos;
   });
-  if (fcg_status st = run_attention(c, layer, meta, false, q, k, v, out, new_pages, (hipStream_t)stream)) return st;
+  if (fcg_status st = run_attention(c, layer, meta, q, k, v, out, new_pages, (hipStream_t)stream)) return st;
   for (int32_t t = 0; t < n_tok; ++t) c->plan.mark(seq[t], layer, pos[t]);
   return FCG_OK;
 }

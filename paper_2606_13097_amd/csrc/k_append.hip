@@ -68,11 +68,11 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const TokenMeta* __res
 }
 
 int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, const void* k, const void* v,
-                       const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws, hipStream_t s) {
+                       const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws, hipStream_t s, KTime tm) {
   if (n == 0) return 0;
   const int rows_ws = n * (Hq / cv.n_kv_heads);
 #define RA(T, DD)                                                                                          \
-  hipLaunchKernelGGL((rope_append_kernel<T, DD>), dim3(n), dim3(256), 0, s, meta, (const T*)q, (const T*)k, \
+  hipExtLaunchKernelGGL((rope_append_kernel<T, DD>), dim3(n), dim3(256), 0, s, tm.start, tm.stop, 0, meta, (const T*)q, (const T*)k, \
                      (const T*)v, cv, layer, inv_freq, Hq, rows_ws, (T*)qws)
   if (dtype == 0) { if (cv.head_dim == 64) RA(float, 64); else RA(float, 128); }
   else { if (cv.head_dim == 64) RA(bf16_t, 64); else RA(bf16_t, 128); }

@@ -314,13 +314,13 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, hipStream_t s) {
+                     int part_stride_rows, hipStream_t s, KTime tm) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
   const bool stage4 = args.span > 2 * kBN;      // splits of more than two tiles stage four per round
 #define PF(DD, PG, WV, ST)                                                                                  \
-  hipLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, ST>), grid, dim3(WV * 64), 0, s, args, meta,     \
+  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, ST>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta,     \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
 #define PFS(DD, PG, WV) { if (stage4) PF(DD, PG, WV, 4); else PF(DD, PG, WV, 2); }
 #define PFW(DD, PG) { if (waves == 8) PFS(DD, PG, 8) else PFS(DD, PG, 4) }

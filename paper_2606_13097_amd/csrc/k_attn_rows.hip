@@ -270,12 +270,12 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restr
 
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
                      int rows_ws, const CacheView& cv, int layer, int Hq, void* out, float* part_o,
-                     float* part_ml, int part_stride_rows, hipStream_t s) {
+                     float* part_ml, int part_stride_rows, hipStream_t s, KTime tm) {
   if (n_items == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
   dim3 grid(n_items, cv.n_kv_heads);
 #define AR(T, DD, GG)                                                                                       \
-  hipLaunchKernelGGL((attn_rows_kernel<T, DD, GG>), grid, dim3(256), 0, s, items, meta, (const T*)qws,      \
+  hipExtLaunchKernelGGL((attn_rows_kernel<T, DD, GG>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, items, meta, (const T*)qws,      \
                      rows_ws, cv, layer, Hq, (T*)out, part_o, part_ml, part_stride_rows)
 #define ARG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
@@ -296,15 +296,15 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq, int Hkv,
                    int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool mfma_part) {
+                   hipStream_t s, bool mfma_part, KTime tm) {
   if (n_items == 0) return 0;
   dim3 grid(n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
 #define CB(T, DD)                                                                                            \
   if (mfma_part)                                                                                             \
-    hipLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o,   \
+    hipExtLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, items, meta, Hq, Hkv, part_o,   \
                        part_ml, part_stride_rows, (T*)out);                                                  \
   else                                                                                                       \
-    hipLaunchKernelGGL((combine_kernel<T, DD, false>), grid, dim3(256), 0, s, items, meta, Hq, Hkv, part_o,  \
+    hipExtLaunchKernelGGL((combine_kernel<T, DD, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, items, meta, Hq, Hkv, part_o,  \
                        part_ml, part_stride_rows, (T*)out)
   if (dtype == 0) { if (D == 64) CB(float, 64); else CB(float, 128); }
   else { if (D == 64) CB(bf16_t, 64); else CB(bf16_t, 128); }

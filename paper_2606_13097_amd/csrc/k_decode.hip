@@ -385,16 +385,16 @@ __global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, cons
 
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
-                  hipStream_t s) {
+                  hipStream_t s, KTime tm) {
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
   dim3 grid(args.max_split, args.n, cv.n_kv_heads);
 #define DK(T, DD, GG)                                                                                       \
   if (cv.page_size)                                                                                         \
-    hipLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, args, (const T*)q,          \
+    hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,          \
                        (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml);             \
   else                                                                                                      \
-    hipLaunchKernelGGL((decode_kernel<T, DD, GG, false>), grid, dim3(256), 0, s, args, (const T*)q,         \
+    hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,         \
                        (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml)
 #define DKG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
@@ -414,12 +414,12 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
 }
 
 int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
-                          const float* part_ml, void* out, hipStream_t s) {
+                          const float* part_ml, void* out, hipStream_t s, KTime tm) {
   if (args.n == 0 || args.max_split <= 1) return 0;
   const int g = Hq / Hkv;
   dim3 grid(args.n, Hkv, g);
 #define DC(T, DD, GG)                                                                                       \
-  hipLaunchKernelGGL((decode_combine_kernel<T, DD, GG>), grid, dim3(DD), 0, s, args, part_o, part_ml, Hkv, (T*)out)
+  hipExtLaunchKernelGGL((decode_combine_kernel<T, DD, GG>), grid, dim3(DD), 0, s, tm.start, tm.stop, 0, args, part_o, part_ml, Hkv, (T*)out)
 #define DCG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
     case 1: DC(T, DD, 1); break;                                                                            \

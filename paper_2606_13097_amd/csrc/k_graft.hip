@@ -135,11 +135,11 @@ int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void
 }
 
 int launch_graft(int dtype, const GraftChunk* chunks, int n_chunks, const void* lib_k, const void* lib_v,
-                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s) {
+                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s, KTime tm) {
   if (n_chunks == 0) return 0;
   dim3 grid(n_chunks, cv.n_kv_heads, L);
 #define GR(T, DD, PG)                                                                                       \
-  hipLaunchKernelGGL((graft_kernel<T, DD, PG>), grid, dim3(256), 0, s, chunks, (const T*)lib_k,             \
+  hipExtLaunchKernelGGL((graft_kernel<T, DD, PG>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, chunks, (const T*)lib_k,             \
                      (const T*)lib_v, cap, cv, inv_freq)
 #define GRD(T, PG) { if (cv.head_dim == 64) GR(T, 64, PG); else GR(T, 128, PG); }
   const bool paged = cv.page_size != 0;

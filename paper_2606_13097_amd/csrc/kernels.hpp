@@ -2,10 +2,18 @@
 // kernels.  Plain structs and pointers only.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace fcg {
+
+// Optional events attached to a kernel's dispatch (hipExtLaunchKernelGGL):
+// they take the kernel's own start and end times, with no extra stream work.
+struct KTime {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
 
 // One run of up to kGraftChunk tokens of one grafted segment.
 struct GraftChunk {
@@ -89,13 +97,13 @@ int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void
                       int Hkv, int D, int64_t cap, int64_t tok_off, hipStream_t s);
 
 int launch_graft(int dtype, const GraftChunk* chunks, int n_chunks, const void* lib_k, const void* lib_v,
-                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s);
+                 int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s, KTime tm = {});
 
 // Encode q and k of n tokens at their positions, store k and v in the cache
 // (layer), write encoded q to qws [Hkv][n * g][D].
 int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, const void* k, const void* v,
                        const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws,
-                       hipStream_t s);
+                       hipStream_t s, KTime tm = {});
 
 // By-value work list of one MFMA prefill launch: row blocks (up to 256 query
 // rows of one sequence), each attended over n_split key splits of `span`
@@ -116,12 +124,12 @@ struct PrefillArgs {
 // bf16 MFMA attention of query-workspace rows over the cache.
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, hipStream_t s);
+                     int part_stride_rows, hipStream_t s, KTime tm = {});
 
 // VALU attention, one token (g query rows) per item; any dtype.
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
                      int rows_ws, const CacheView& cv, int layer, int Hq, void* out, float* part_o,
-                     float* part_ml, int part_stride_rows, hipStream_t s);
+                     float* part_ml, int part_stride_rows, hipStream_t s, KTime tm = {});
 
 // Decode step: encode + store the new token and split-KV attention over the
 // cache.  q, k, v, out: [n][H][D] rows in the order of args.seq.  Grid
@@ -130,16 +138,16 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 // split, merged by launch_decode_combine.
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
-                  hipStream_t s);
+                  hipStream_t s, KTime tm = {});
 
 // Merge the decode partials of the multi-split sequences of args into out.
 int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
-                          const float* part_ml, void* out, hipStream_t s);
+                          const float* part_ml, void* out, hipStream_t s, KTime tm = {});
 
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
 // accumulator order of the MFMA prefill kernel.
 int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
                    int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool mfma_part = false);
+                   hipStream_t s, bool mfma_part = false, KTime tm = {});
 
 }  // namespace fcg

@@ -36,7 +36,7 @@ EXPORTS = [
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
     "fcg_cache_timing", "fcg_cache_timing_read",
 ]
-FCG_TIME_GRAFT, FCG_TIME_PREFILL_ATTN, FCG_TIME_PREFILL, FCG_TIME_DECODE = range(4)
+FCG_TIME_GRAFT, FCG_TIME_PREFILL_ATTN, FCG_TIME_PREFILL, FCG_TIME_DECODE, FCG_TIME_DECODE_ATTN = range(5)
 
 
 class FcgError(RuntimeError):

@@ -50,8 +50,8 @@ def test_timing_api_without_device_work():
     c = fcg.Cache(fcg.model_desc(1, 4, 2, 64, 1e4, "f32"), 1, 32, flags=fcg.FCG_LAYOUT_ONLY)
     fcg.fcg_cache_timing(c, True)
     fcg.fcg_patch_prefill(c, 0, [0, 0], [0, 1], None, None, None, None)
-    for kind in range(4):
+    for kind in range(5):
         assert fcg.fcg_cache_timing_read(c, kind) == (0, 0.0)
     with pytest.raises(fcg.FcgError) as e:
-        fcg.fcg_cache_timing_read(c, 4)
+        fcg.fcg_cache_timing_read(c, 5)
     assert e.value.status == fcg.FCG_ERANGE

@@ -301,9 +301,10 @@ def test_kernel_timing_counts_calls():
         dq, dk, dv = s.decode_inputs(0, 3)
         for t in range(3):
             s.decode(0, dq[t], dk[t], dv[t], torch.empty_like(dq[t]))
-        counts = [fcg.fcg_cache_timing_read(s.cache, k) for k in range(4)]
-        assert [c[0] for c in counts] == [1, 2, 2, 3]
+        counts = [fcg.fcg_cache_timing_read(s.cache, k) for k in range(5)]
+        assert [c[0] for c in counts] == [1, 2, 2, 3, 3]
         assert all(c[1] > 0 for c in counts)
         assert counts[2][1] >= counts[1][1]            # the whole prefill includes its attention kernel
+        assert counts[3][1] >= counts[4][1]            # the whole decode includes its attention kernel
     finally:
         s.close()
