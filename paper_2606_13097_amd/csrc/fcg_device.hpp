@@ -66,6 +66,14 @@ __device__ __forceinline__ uint4 ld16_nt(const void* p) {
   const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
 }
+
+// 8-byte store with the nontemporal hint: for results another kernel reads
+// (from another XCD's L2, so keeping them in this one buys nothing)
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void st8_nt(void* p, uint32_t lo, uint32_t hi) {
+  const u32x2_t v = {lo, hi};
+  __builtin_nontemporal_store(v, reinterpret_cast<u32x2_t*>(p));
+}
 __device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
 
 // cos and sin of pos * w for the rotary pair with float64 frequency w: the

@@ -295,14 +295,15 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
     } else {
       // partial outputs in bf16 (the merge weights them in fp32; they end in
       // bf16), stored in accumulator order: per 16-row and 16-dim tile the 64
-      // lanes' 4 values, so every store covers 512 contiguous bytes
+      // lanes' 4 values, so every store covers 512 contiguous bytes; streaming
+      // stores, read once by the merge kernel
       const int64_t pr = ((int64_t)part * Hkv + hk) * part_stride_rows + r;
       bf16_t* o = reinterpret_cast<bf16_t*>(part_o) + ((int64_t)part * Hkv + hk) * part_stride_rows * D +
                   ((int64_t)(2 * w + rt) * DT * 64 + lane) * 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 a = acc[rt][dt];
-        *reinterpret_cast<uint2*>(o + dt * 256) = make_uint2(cvt_bf16x2(a[0], a[1]), cvt_bf16x2(a[2], a[3]));
+        st8_nt(o + dt * 256, cvt_bf16x2(a[0], a[1]), cvt_bf16x2(a[2], a[3]));
       }
       if (lq == 0) {
         part_ml[pr * 2 + 0] = mrow[rt];
