@@ -137,11 +137,12 @@ class Library:
         h = C.c_void_p()
         _check(_L.fcg_lib_create(C.byref(desc), int(capacity_tokens), int(max_segments), int(flags), C.byref(h)))
         self.h, self.desc = h, desc
+        self._lib = _L   # kept for close(), which may run while the interpreter tears down globals
         self.capacity = int(capacity_tokens)
 
     def close(self):
         if self.h:
-            _L.fcg_lib_destroy(self.h)
+            self._lib.fcg_lib_destroy(self.h)
             self.h = None
 
     __del__ = close
@@ -158,12 +159,13 @@ class Cache:
         _check(_L.fcg_cache_create(C.byref(desc), int(n_seqs), int(max_tokens), int(page_size), int(n_pages),
                                    int(flags), C.byref(h)))
         self.h, self.desc = h, desc
+        self._lib = _L   # kept for close(), which may run while the interpreter tears down globals
         self.n_seqs, self.max_tokens, self.page_size, self.n_pages = n_seqs, max_tokens, page_size, n_pages
         self.n_lp = -(-max_tokens // page_size) if page_size else 0
 
     def close(self):
         if self.h:
-            _L.fcg_cache_destroy(self.h)
+            self._lib.fcg_cache_destroy(self.h)
             self.h = None
 
     __del__ = close

@@ -405,6 +405,20 @@ def workload(name: str, seed: int = 1, *, n_layers: Optional[int] = None,
 WORKLOADS: List[str] = ["tiny", "7b", "long16k", "batched", "34b"]
 
 
+def custom(shape: Shape, seed: int, lengths, seq_segments, n_fresh: int, n_decode: int, *,
+           page_size: int = 0, kv_scale: float = 0.5, name: str = "custom") -> Workload:
+    """A hand-made workload for edge cases: sequence i grafts the segments
+    ``seq_segments[i]`` back to back from position 0, then ``n_fresh`` fresh
+    tokens follow, then ``n_decode`` decode steps."""
+    graft, fresh = [], []
+    for seq, segs in enumerate(seq_segments):
+        items, pos = _consecutive_task(seq, list(segs), lengths, 0)
+        graft += items
+        fresh += [(seq, pos + j, j) for j in range(n_fresh)]
+    return _finish(name, shape, seed, list(lengths), kv_scale, 1.0, 0.0, page_size, graft, fresh, n_decode,
+                   len(seq_segments))
+
+
 # ----------------------------------------------------------------------------
 # Convenience: host values of the tensors a workload feeds the path
 # ----------------------------------------------------------------------------

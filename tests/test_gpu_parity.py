@@ -308,3 +308,17 @@ def test_kernel_timing_counts_calls():
         assert counts[3][1] >= counts[4][1]            # the whole decode includes its attention kernel
     finally:
         s.close()
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("hq,hkv,d,dtype", [(32, 8, 128, "bf16"), (64, 8, 128, "bf16"), (8, 4, 64, "bf16"),
+                                            (4, 2, 64, "f32")])
+def test_decode_split_edges(hq, hkv, d, dtype):
+    """Decode positions on and next to the 64-key split boundaries (a last split holding only
+    the new token, a split ending on the last cached key), in a batch whose sequences have
+    different split counts (empty padding splits), plus three-token prefills."""
+    from paper_2606_13097_amd import synth
+    shape = synth.Shape(1, hq, hkv, d, 1e4, dtype)
+    lengths = [58, 61, 124, 125, 197, 252]       # contexts 61, 64, 127, 128, 200, 255 after 3 fresh tokens
+    w = synth.custom(shape, 11, lengths, [[i] for i in range(len(lengths))], n_fresh=3, n_decode=3)
+    run_pipeline(w, [0], 3, list(range(w.n_seqs)))
