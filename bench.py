@@ -161,9 +161,16 @@ def main():
     out_d = torch.empty_like(dec[0][0][0])
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
     cache = setup.cache
     lib = setup.lib
-    all_seqs = np.arange(w.n_seqs)
+    all_seqs = np.arange(w.n_seqs, dtype=np.int32)
+    # device addresses of every call's tensors, taken once: the loop below is
+    # the library's calls, not the creation of tensor views
+    fresh_p = [tuple(t.data_ptr() for t in fresh[l]) + (outs_p[l].data_ptr(),) for l in range(sh.n_layers)]
+    dec_p = [[(dec[l][0][t].data_ptr(), dec[l][1][t].data_ptr(), dec[l][2][t].data_ptr())
+              for l in range(sh.n_layers)] for t in range(w.n_decode)]
+    out_dp = out_d.data_ptr()
 
     def ev():
         e = torch.cuda.Event(enable_timing=True)
@@ -174,16 +181,16 @@ def main():
         for s in range(w.n_seqs):
             fcg.fcg_cache_reset(cache, s)
         e0 = ev()
-        fcg.fcg_graft(cache, lib, tw.graft_seq, tw.graft_seg, tw.graft_dst)
+        fcg.fcg_graft(cache, lib, tw.graft_seq, tw.graft_seg, tw.graft_dst, sp)
         e1 = ev()
         for l in range(sh.n_layers):
-            q, k, v = fresh[l]
-            fcg.fcg_patch_prefill(cache, l, tw.fresh_seq, tw.fresh_pos, q, k, v, outs_p[l])
+            q, k, v, o = fresh_p[l]
+            fcg.fcg_patch_prefill(cache, l, tw.fresh_seq, tw.fresh_pos, q, k, v, o, sp)
         e2 = ev()
         for t in range(tw.n_decode):
             for l in range(sh.n_layers):
-                dq, dk, dv = dec[l]
-                fcg.fcg_decode(cache, l, all_seqs, dq[t], dk[t], dv[t], out_d)
+                dq, dk, dv = dec_p[t][l]
+                fcg.fcg_decode(cache, l, all_seqs, dq, dk, dv, out_dp, sp)
         e3 = ev()
         return e0, e1, e2, e3
 
@@ -212,7 +219,7 @@ def main():
     fcg.fcg_cache_timing(cache, False)
     kt = {k: fcg.fcg_cache_timing_read(cache, k) for k in range(5)}
 
-    g_bytes = g_ms = p_flops = p_ms = d_bytes = d_ms = 0.0
+    g_bytes = g_ms = p_flops = p_bytes = p_ms = d_bytes = d_ms = 0.0
     n_dec_calls = 0
     kvb = 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes          # K+V bytes of one token in one layer
     for tw, (e0, e1, e2, e3) in marks:
@@ -221,6 +228,10 @@ def main():
         d_ms += e2.elapsed_time(e3)
         g_bytes += 2 * tw.grafted_tokens * kvb * sh.n_layers
         p_flops += 4 * sh.n_q_heads * sh.head_dim * float((tw.fresh_pos.astype(np.int64) + 1).sum()) * sh.n_layers
+        # HBM bytes the attention must move: the visible keys and values once, the
+        # encoded queries in and the outputs out
+        qo = 2 * len(tw.fresh_pos) * sh.n_q_heads * sh.head_dim * sh.elem_bytes
+        p_bytes += (tw.seq_len_after_prefill(0) * kvb + qo) * sh.n_layers
         ctx = tw.seq_len_after_prefill(0)
         d_bytes += sum((ctx + t + 1) * kvb for t in range(tw.n_decode)) * sh.n_layers
         n_dec_calls += tw.n_decode * sh.n_layers
@@ -230,6 +241,10 @@ def main():
     assert nda == n_dec_calls, kt
     graft_gbs = g_bytes / (g_kms / 1e3) / 1e9                  # graft kernel
     attn_tflops = p_flops / (a_kms / 1e3) / 1e12               # MFMA attention kernel
+    attn_gbs = p_bytes / (a_kms / 1e3) / 1e9
+    # roofline of the attention kernel: attainable = min(MFMA peak, intensity x HBM peak)
+    p_intensity = p_flops / p_bytes
+    p_bound = "mfma" if p_intensity * HBM_PEAK_GBS / 1e3 >= BF16_PEAK_TFLOPS else "hbm"
     prefill_tflops = p_flops / (p_kms / 1e3) / 1e12            # append + attention + merge kernels
     decode_gbs = d_bytes / (d_kms / 1e3) / 1e9                 # decode + merge kernels
     decode_attn_gbs = d_bytes / (da_kms / 1e3) / 1e9           # decode attention kernel
@@ -276,11 +291,18 @@ def main():
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(graft_gbs / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("graft_7b_traffic.json"),
                      "algorithmic_bytes_per_launch": int(round(g_bytes / K))},
-        "roofline_patch_attn": {"bound": "mfma", "kernel": "fcg attn_prefill_mfma_kernel",
-                                "achieved": round(attn_tflops, 3), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                                "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
-                                "traffic": measured_traffic("prefill_7b_traffic.json"),
-                                "algorithmic_flops_per_launch": int(round(p_flops / (K * sh.n_layers)))},
+        "roofline_patch_attn": (
+            {"bound": "hbm", "kernel": "fcg attn_prefill_mfma_kernel", "achieved": round(attn_gbs, 2),
+             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(attn_gbs / HBM_PEAK_GBS, 4)}
+            if p_bound == "hbm" else
+            {"bound": "mfma", "kernel": "fcg attn_prefill_mfma_kernel", "achieved": round(attn_tflops, 3),
+             "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)}) | {
+            "traffic": measured_traffic("prefill_7b_traffic.json"),
+            "algorithmic_flops_per_launch": int(round(p_flops / (K * sh.n_layers))),
+            "algorithmic_bytes_per_launch": int(round(p_bytes / (K * sh.n_layers))),
+            "intensity_flop_per_byte": round(p_intensity, 1),
+            "mfma_frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
+            "hbm_frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
         "roofline_decode": {"bound": "hbm", "kernel": "fcg decode_kernel", "achieved": round(decode_attn_gbs, 2),
                             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_attn_gbs / HBM_PEAK_GBS, 4),
                             "traffic": measured_traffic("decode_7b_traffic.json"),

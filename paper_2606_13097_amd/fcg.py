@@ -61,7 +61,7 @@ def _load():
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_13097_amd.build`")
     lib = C.CDLL(LIB_PATH)
     P, I32, I64, U32 = C.c_void_p, C.c_int32, C.c_int64, C.c_uint32
-    PI32, PI64, PU8 = C.POINTER(C.c_int32), C.POINTER(C.c_int64), C.POINTER(C.c_uint8)
+    PI32, PI64 = C.POINTER(C.c_int32), C.POINTER(C.c_int64)
     sig = {
         "fcg_lib_create": [C.POINTER(ModelDesc), I64, I32, U32, C.POINTER(P)],
         "fcg_lib_add_segment": [P, I32, I32, P, P, P, PI32],
@@ -70,12 +70,13 @@ def _load():
         "fcg_lib_destroy": [P],
         "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
         "fcg_cache_reset": [P, I32],
-        "fcg_cache_export_layout": [P, I32, I32, PI32, PI32, PU8],
+        "fcg_cache_export_layout": [P, I32, I32, P, PI32, P],
         "fcg_cache_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
         "fcg_cache_destroy": [P],
-        "fcg_graft": [P, P, I32, PI32, PI32, PI32, P],
-        "fcg_patch_prefill": [P, I32, I32, PI32, PI32, P, P, P, P, P],
-        "fcg_decode": [P, I32, I32, PI32, P, P, P, P, PI32, P],
+        # int32 arrays go as plain addresses (ndarray.ctypes.data): no pointer objects per call
+        "fcg_graft": [P, P, I32, P, P, P, P],
+        "fcg_patch_prefill": [P, I32, I32, P, P, P, P, P, P, P],
+        "fcg_decode": [P, I32, I32, P, P, P, P, P, P, P],
         "fcg_cache_timing": [P, I32],
         "fcg_cache_timing_read": [P, I32, PI32, C.POINTER(C.c_double)],
     }
@@ -103,7 +104,7 @@ def _i32(a) -> np.ndarray:
 
 
 def _p(a: np.ndarray):
-    return a.ctypes.data_as(C.POINTER(C.c_int32)) if a.size else None
+    return a.ctypes.data if a.size else None
 
 
 def _dptr(t) -> Optional[int]:
@@ -114,15 +115,20 @@ def _dptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
+def _current_stream() -> Optional[int]:
+    """Raw handle of torch's current stream on the current device (None without a GPU)."""
+    import torch
+    if not torch.cuda.is_available():
+        return None
+    raw = getattr(torch._C, "_cuda_getCurrentRawStream", None)   # no Stream object per call
+    if raw is not None:
+        return raw(torch.cuda.current_device())
+    return torch.cuda.current_stream().cuda_stream
+
+
 def _stream(stream) -> Optional[int]:
     if stream is None:
-        try:
-            import torch
-            if torch.cuda.is_available():
-                return torch.cuda.current_stream().cuda_stream
-        except Exception:
-            pass
-        return None
+        return _current_stream()
     if isinstance(stream, int):
         return stream
     return stream.cuda_stream
@@ -213,7 +219,7 @@ def fcg_cache_export_layout(cache: Cache, seq: int, layer: int):
     n = C.c_int32()
     wr = np.zeros(cache.max_tokens, dtype=np.uint8)
     _check(_L.fcg_cache_export_layout(cache.h, int(seq), int(layer), _p(pt) if cache.page_size else None,
-                                      C.byref(n), wr.ctypes.data_as(C.POINTER(C.c_uint8))))
+                                      C.byref(n), wr.ctypes.data))
     return (pt[:cache.n_lp] if cache.page_size else None), n.value, wr
 
 
@@ -247,7 +253,7 @@ def fcg_decode(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.
     s = _i32(seqs)
     pos = np.zeros(max(s.size, 1), dtype=np.int32)
     _check(_L.fcg_decode(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
-                         pos.ctypes.data_as(C.POINTER(C.c_int32)), _stream(stream) if q is not None else None))
+                         pos.ctypes.data, _stream(stream) if q is not None else None))
     return pos[:s.size]
 
 
