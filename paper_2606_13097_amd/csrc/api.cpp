@@ -612,19 +612,28 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     rblocks.push_back({r, u - r});
     r = u;
   }
-  // split the key range of each row block so that the grid covers the chip about once
+  // split the key range of each row block so that the grid covers the chip
+  // once: one split length (in tiles) for the call, the smallest whose blocks
+  // fit one per CU; at most 256 splits per row block (the merge table)
   const int tile = mfma ? 64 : 256;
-  int64_t total_tiles = 0;
-  for (auto& rb : rblocks) total_tiles += (meta[rb.first + rb.second - 1].pos + tile) / tile;
-  const int64_t target = std::max<int64_t>(1, 256 / d.n_kv_heads);
-  const int min_tiles = mfma ? 2 : 1;
-  const int64_t per = std::max<int64_t>(min_tiles, (total_tiles + target - 1) / target);
-  // one split length for the call (at most 256 splits per row block: the merge table)
-  int64_t span = per * tile;
+  std::vector<int64_t> rb_tiles;
+  int64_t total_tiles = 0, max_tiles = 0;
   for (auto& rb : rblocks) {
-    const int kend = meta[rb.first + rb.second - 1].pos + 1;
-    span = std::max<int64_t>(span, ((kend + 255) / 256 + tile - 1) / tile * tile);
+    rb_tiles.push_back((meta[rb.first + rb.second - 1].pos + tile) / tile);
+    total_tiles += rb_tiles.back();
+    max_tiles = std::max(max_tiles, rb_tiles.back());
   }
+  const int64_t target = 256;
+  const int min_tiles = mfma ? 2 : 1;
+  int64_t per = std::max<int64_t>({(int64_t)min_tiles, (total_tiles * d.n_kv_heads + target - 1) / target,
+                                   (max_tiles + 255) / 256});
+  for (;;) {
+    int64_t blocks = 0;
+    for (int64_t nt : rb_tiles) blocks += (nt + per - 1) / per;
+    if (blocks * d.n_kv_heads <= target || per >= max_tiles) break;
+    ++per;
+  }
+  const int64_t span = per * tile;
   std::vector<AttnItem> items;                 // VALU path: one item per (row block, split)
   std::vector<PrefillRb> pf_rb;                // MFMA path: row blocks, items built per launch
   std::vector<int> pf_nsplit;
