@@ -684,7 +684,6 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   stage_pages(c, new_pages, &blob, &rows);
   const size_t o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
   const size_t o_items = mfma ? 0 : blob.add(items.data(), items.size() * sizeof(AttnItem));
-  const size_t o_comb = blob.add(comb.data(), comb.size() * sizeof(CombineItem));
   char* dev;
   size_t off;
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
@@ -710,9 +709,13 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     rc = launch_attn_rows(d.dtype, (const AttnItem*)(dev + o_items), (int)items.size(), dmeta, c->qws, n * g, cv,
                           layer, d.n_q_heads, out, part_o, part_ml, stride_rows, s, KTime{e_attn0, e_attn1});
   if (rc) return hip_fail((hipError_t)rc, "attention launch");
-  if (!comb.empty()) {
-    rc = launch_combine(d.dtype, (const CombineItem*)(dev + o_comb), (int)comb.size(), dmeta, d.n_q_heads,
-                        d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows, out, s, mfma, KTime{nullptr, e_call1});
+  for (size_t c0 = 0; c0 < comb.size(); c0 += kCombMaxItems) {  // merge plans by value
+    CombineArgs ca{};
+    ca.n_items = (int32_t)std::min<size_t>(kCombMaxItems, comb.size() - c0);
+    std::copy(comb.begin() + c0, comb.begin() + c0 + ca.n_items, ca.item);
+    const bool last = c0 + kCombMaxItems >= comb.size();
+    rc = launch_combine(d.dtype, ca, dmeta, d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml, stride_rows,
+                        out, s, mfma, KTime{nullptr, last ? e_call1 : nullptr});
     if (rc) return hip_fail((hipError_t)rc, "combine launch");
   }
   if (mfma && pf_launch.empty()) {  // nothing attended: no attention interval

@@ -25,45 +25,77 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const TokenMeta* __res
   __shared__ float s_cos[HALF], s_sin[HALF];
 
   const int r = blockIdx.x;
+  const int t = threadIdx.x;
   const TokenMeta m = meta[r];
   const int Hkv = cv.n_kv_heads;
   const int g = Hq / Hkv;
-  if (threadIdx.x < HALF) rope_cs((double)m.pos, inv_freq[threadIdx.x], &s_cos[threadIdx.x], &s_sin[threadIdx.x]);
-  __syncthreads();
-
   T* ck = reinterpret_cast<T*>(cv.k);
   T* cvv = reinterpret_cast<T*>(cv.v);
   const int n_q = Hq * KT, n_k = Hkv * KT, n_v = Hkv * VT;
-  for (int i = threadIdx.x; i < n_q + n_k + n_v; i += blockDim.x) {
+  const int total = n_q + n_k + n_v;
+  // item i: a q or k rotary chunk (i < n_q + n_k) or a v chunk; the source of
+  // each item (both halves of a rotary pair) is loaded before the rotary table
+  // is built, so the two latencies overlap
+  auto src_of = [&](int i, const T** p) -> bool {  // -> is a rotary item
     if (i < n_q + n_k) {
       const bool is_q = i < n_q;
       const int ii = is_q ? i : i - n_q;
       const int head = ii / KT, c = ii % KT;
-      const T* src = is_q ? q + ((int64_t)m.tok * Hq + head) * D : k + ((int64_t)m.tok * Hkv + head) * D;
+      *p = (is_q ? q + ((int64_t)m.tok * Hq + head) * D : k + ((int64_t)m.tok * Hkv + head) * D) + c * VEC;
+      return true;
+    }
+    const int ii = i - n_q - n_k;
+    *p = v + ((int64_t)m.tok * Hkv + ii / VT) * D + (ii % VT) * VEC;
+    return false;
+  };
+  auto finish = [&](int i, const uint4& a, const uint4& b) {
+    if (i < n_q + n_k) {
+      const bool is_q = i < n_q;
+      const int ii = is_q ? i : i - n_q;
+      const int head = ii / KT, c = ii % KT;
       float x1[VEC], x2[VEC], y1[VEC], y2[VEC];
-      Store<T>::unpack(ld16(src + c * VEC), x1);
-      Store<T>::unpack(ld16(src + HALF + c * VEC), x2);
+      Store<T>::unpack(a, x1);
+      Store<T>::unpack(b, x2);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) {
         const float cs = s_cos[c * VEC + e], sn = s_sin[c * VEC + e];
         y1[e] = fmaf(x1[e], cs, -x2[e] * sn);
         y2[e] = fmaf(x2[e], cs, x1[e] * sn);
       }
-      T* dst;
-      if (is_q) {
-        const int hk = head / g, j = head % g;
-        dst = qws + ((int64_t)hk * rows_ws + (int64_t)r * g + j) * D;
-      } else {
-        dst = ck + cache_offset(cv, layer, m.seq, head, m.pos);
-      }
+      T* dst = is_q ? qws + ((int64_t)(head / g) * rows_ws + (int64_t)r * g + head % g) * D
+                    : ck + cache_offset(cv, layer, m.seq, head, m.pos);
       st16(dst + c * VEC, Store<T>::pack(y1));
       st16(dst + HALF + c * VEC, Store<T>::pack(y2));
     } else {
       const int ii = i - n_q - n_k;
-      const int head = ii / VT, c = ii % VT;
-      const int64_t off = cache_offset(cv, layer, m.seq, head, m.pos);
-      st16(cvv + off + c * VEC, ld16(v + ((int64_t)m.tok * Hkv + head) * D + c * VEC));
+      st16(cvv + cache_offset(cv, layer, m.seq, ii / VT, m.pos) + (ii % VT) * VEC, a);
     }
+  };
+  constexpr int PRE = 3;  // items per lane loaded up front (all of them up to 64 query heads at D 128)
+  uint4 pa[PRE], pb[PRE];
+#pragma unroll
+  for (int p = 0; p < PRE; ++p) {
+    const int i = t + p * 256;
+    if (i < total) {
+      const T* src;
+      const bool rot = src_of(i, &src);
+      pa[p] = ld16(src);
+      pb[p] = rot ? ld16(src + HALF) : pa[p];
+    }
+  }
+  const double w = inv_freq[t % HALF];
+  if (t < HALF) rope_cs((double)m.pos, w, &s_cos[t], &s_sin[t]);
+  __syncthreads();
+#pragma unroll
+  for (int p = 0; p < PRE; ++p) {
+    const int i = t + p * 256;
+    if (i < total) finish(i, pa[p], pb[p]);
+  }
+  for (int i = t + PRE * 256; i < total; i += 256) {
+    const T* src;
+    const bool rot = src_of(i, &src);
+    const uint4 a = ld16(src);
+    finish(i, a, rot ? ld16(src + HALF) : a);
   }
 }
 

@@ -156,50 +156,36 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
 
 // Merge split-KV partials: per row, M = max M_s, L = sum L_s 2^(M_s - M),
 // O = sum O_s 2^(M_s - M) / L.  Block (row block, kv head, z) merges up to
-// kCombRows rows: every lane first fetches one (M_s, L_s) pair into LDS (all
-// pairs in flight at once), the scale 2^(M_s - M) / L of every split is formed
-// there, then the 4-dim output chunks are summed over the splits with
-// 16-byte loads, LPC lanes per chunk taking interleaved splits, and the LPC
-// sums are added through LDS.
+// kCombRows rows, its item taken from the by-value plan.  Every load that
+// does not depend on another is issued first: the (M_s, L_s) pairs into LDS,
+// the rows' output tokens and, for the bf16 MFMA partials, the first
+// kCombPre splits' partial outputs of the lane's 4-dim chunk; 32 lanes per
+// row then form the scales 2^(M_s - M) / L with shuffles, and each 4-dim
+// output chunk is summed over the splits (fp32 partials: LPC lanes per chunk
+// taking interleaved splits, their sums added through LDS).
 constexpr int kCombRows = 8;
 constexpr int kCombMaxParts = 256;
+constexpr int kCombPre = 32;
 
 template <typename T, int D, bool MFMA_PART>
-__global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restrict__ items,
-                                                      const TokenMeta* __restrict__ meta, int Hq, int Hkv,
-                                                      const float* __restrict__ part_o,
+__global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const TokenMeta* __restrict__ meta, int Hq,
+                                                      int Hkv, const float* __restrict__ part_o,
                                                       const float* __restrict__ part_ml, int part_stride_rows,
                                                       T* __restrict__ out) {
   __shared__ float s_f[kCombRows][kCombMaxParts + 1];  // +1: rows start in different banks
+  __shared__ float s_l[kCombRows][kCombMaxParts + 1];
   __shared__ float4 s_acc[256];
-  const CombineItem it = items[blockIdx.x];
+  const CombineItem it = args.item[blockIdx.x];
   const int hk = blockIdx.y;
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
   const int r0 = blockIdx.z * kCombRows;
   const int nr = min(kCombRows, it.n_rank * g - r0);
-  if (nr <= 0) return;
   const int np = it.n_part;
+  asm volatile("" ::"s"(it.rank0), "s"(nr), "s"(np), "s"(it.part0), "s"(meta), "s"(part_o), "s"(part_ml),
+               "s"(out), "s"(Hq), "s"(Hkv), "s"(part_stride_rows));
+  if (nr <= 0) return;
   auto prow = [&](int s, int r) { return ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + r0 + r; };
-  for (int idx = t; idx < nr * np; idx += 256) {
-    const int r = idx / np, s = idx % np;
-    s_f[r][s] = part_ml[prow(s, r) * 2];
-  }
-  __syncthreads();
-  if (t < nr) {
-    float M = -INFINITY;
-    for (int s = 0; s < np; ++s) M = fmaxf(M, s_f[t][s]);
-    float L = 0.f;
-    for (int s = 0; s < np; ++s) {
-      const float ms = s_f[t][s];
-      const float f = ms == -INFINITY ? 0.f : exp2f(ms - M);
-      s_f[t][s] = f;
-      L = fmaf(part_ml[prow(s, t) * 2 + 1], f, L);
-    }
-    const float inv = L > 0.f ? 1.f / L : 0.f;
-    for (int s = 0; s < np; ++s) s_f[t][s] *= inv;
-  }
-  __syncthreads();
   constexpr int CPR = D / 4;                  // 4-dim chunks per row
   const int nch = nr * CPR;
   const int lpc = max(1, 256 / nch);          // lanes per chunk (power of two: nr, CPR are)
@@ -209,63 +195,95 @@ __global__ void __launch_bounds__(256) combine_kernel(const CombineItem* __restr
     *r = MFMA_PART ? c % nr : c / CPR;
     *c4 = MFMA_PART ? c / nr : c % CPR;
   };
-  for (int c = t / lpc; c < nch; c += 256 / lpc) {
-    const int sub = t % lpc;
-    int r, c4;
-    chunk(c, &r, &c4);
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll 8
-    for (int s = sub; s < np; s += lpc) {
-      const float f = s_f[r][s];
-      float4 o;
-      if (MFMA_PART) {
-        // bf16, in the MFMA accumulator order of the prefill kernel: per
-        // 16-row tile and 16-dim tile, 64 lanes x 4 dims, lane = row % 16 +
-        // 16 * (4-dim chunk % 4)
-        const int rr = r0 + r;
-        const int64_t off = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows * D +
-                            (((rr / 16) * (D / 16) + c4 / 4) * 64 + rr % 16 + 16 * (c4 % 4)) * 4;
-        const uint2 u = *reinterpret_cast<const uint2*>(reinterpret_cast<const bf16_t*>(part_o) + off);
-        o = make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y));
-      } else {
-        o = *reinterpret_cast<const float4*>(part_o + prow(s, r) * D + c4 * 4);
+  // bf16 partial output of split s, row r, chunk c4, in the MFMA accumulator
+  // order of the prefill kernel: per 16-row tile and 16-dim tile, 64 lanes x
+  // 4 dims, lane = row % 16 + 16 * (4-dim chunk % 4)
+  auto mfma_part = [&](int s, int r, int c4) -> uint2 {
+    const int rr = r0 + r;
+    const int64_t off = ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows * D +
+                        (((rr / 16) * (D / 16) + c4 / 4) * 64 + rr % 16 + 16 * (c4 % 4)) * 4;
+    return *reinterpret_cast<const uint2*>(reinterpret_cast<const bf16_t*>(part_o) + off);
+  };
+  int my_r = 0, my_c4 = 0;
+  const bool my_chunk = t / lpc < nch;
+  chunk(my_chunk ? t / lpc : 0, &my_r, &my_c4);
+  uint2 pre[MFMA_PART ? kCombPre : 1];
+  if (MFMA_PART) {
+    // lpc is 1 here (nch = 8 rows x D/4 chunks = 256 lanes for a full block)
+#pragma unroll
+    for (int u = 0; u < kCombPre; ++u) pre[u] = mfma_part(min(u, np - 1), my_r, my_c4);
+  }
+  const TokenMeta mt = meta[it.rank0 + (r0 + my_r) / g];
+  for (int idx = t; idx < nr * np; idx += 256) {
+    const int r = idx / np, s = idx % np;
+    s_f[r][s] = part_ml[prow(s, r) * 2];
+    s_l[r][s] = part_ml[prow(s, r) * 2 + 1];
+  }
+  __syncthreads();
+  {
+    // 32 lanes per row: M, L and the scales 2^(M_s - M) / L
+    const int r = t / 32, l32 = t % 32;
+    if (r < nr) {
+      float M = -INFINITY;
+      for (int s = l32; s < np; s += 32) M = fmaxf(M, s_f[r][s]);
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 32));
+      float L = 0.f;
+      for (int s = l32; s < np; s += 32) {
+        const float ms = s_f[r][s];
+        L = fmaf(s_l[r][s], ms == -INFINITY ? 0.f : exp2f(ms - M), L);
       }
-      acc.x = fmaf(o.x, f, acc.x);
-      acc.y = fmaf(o.y, f, acc.y);
-      acc.z = fmaf(o.z, f, acc.z);
-      acc.w = fmaf(o.w, f, acc.w);
+#pragma unroll
+      for (int o = 16; o >= 1; o >>= 1) L += __shfl_xor(L, o, 32);
+      const float inv = L > 0.f ? 1.f / L : 0.f;
+      for (int s = l32; s < np; s += 32) {
+        const float ms = s_f[r][s];
+        s_f[r][s] = ms == -INFINITY ? 0.f : exp2f(ms - M) * inv;
+      }
+    }
+  }
+  __syncthreads();
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto add = [&](float4 o, float f) {
+    acc.x = fmaf(o.x, f, acc.x);
+    acc.y = fmaf(o.y, f, acc.y);
+    acc.z = fmaf(o.z, f, acc.z);
+    acc.w = fmaf(o.w, f, acc.w);
+  };
+  auto bf4 = [](uint2 u) { return make_float4(lo_bf16(u.x), hi_bf16(u.x), lo_bf16(u.y), hi_bf16(u.y)); };
+  if (MFMA_PART) {
+    if (!my_chunk) return;
+#pragma unroll
+    for (int u = 0; u < kCombPre; ++u)
+      if (u < np) add(bf4(pre[u]), s_f[my_r][u]);
+#pragma unroll 8
+    for (int s = kCombPre; s < np; ++s) add(bf4(mfma_part(s, my_r, my_c4)), s_f[my_r][s]);
+  } else {
+    if (my_chunk) {
+#pragma unroll 8
+      for (int s = t % lpc; s < np; s += lpc)
+        add(*reinterpret_cast<const float4*>(part_o + prow(s, my_r) * D + my_c4 * 4), s_f[my_r][s]);
     }
     if (lpc > 1) {
       s_acc[t] = acc;
-    } else {
-      const TokenMeta m = meta[it.rank0 + (r0 + r) / g];
-      T* dst = out + ((int64_t)m.tok * Hq + hk * g + (r0 + r) % g) * D + c4 * 4;
-      Store<T>::store1(dst + 0, acc.x);
-      Store<T>::store1(dst + 1, acc.y);
-      Store<T>::store1(dst + 2, acc.z);
-      Store<T>::store1(dst + 3, acc.w);
+      __syncthreads();
+      if (t % lpc || !my_chunk) return;
+      for (int sub = 1; sub < lpc; ++sub) {
+        const float4 a4 = s_acc[t + sub];
+        acc.x += a4.x;
+        acc.y += a4.y;
+        acc.z += a4.z;
+        acc.w += a4.w;
+      }
+    } else if (!my_chunk) {
+      return;
     }
   }
-  if (lpc == 1) return;
-  __syncthreads();
-  if (t < nch) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int sub = 0; sub < lpc; ++sub) {
-      const float4 a4 = s_acc[t * lpc + sub];
-      acc.x += a4.x;
-      acc.y += a4.y;
-      acc.z += a4.z;
-      acc.w += a4.w;
-    }
-    int r, c4;
-    chunk(t, &r, &c4);
-    const TokenMeta m = meta[it.rank0 + (r0 + r) / g];
-    T* dst = out + ((int64_t)m.tok * Hq + hk * g + (r0 + r) % g) * D + c4 * 4;
-    Store<T>::store1(dst + 0, acc.x);
-    Store<T>::store1(dst + 1, acc.y);
-    Store<T>::store1(dst + 2, acc.z);
-    Store<T>::store1(dst + 3, acc.w);
-  }
+  T* dst = out + ((int64_t)mt.tok * Hq + hk * g + (r0 + my_r) % g) * D + my_c4 * 4;
+  Store<T>::store1(dst + 0, acc.x);
+  Store<T>::store1(dst + 1, acc.y);
+  Store<T>::store1(dst + 2, acc.z);
+  Store<T>::store1(dst + 3, acc.w);
 }
 
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
@@ -294,18 +312,18 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
   return e == hipSuccess ? 0 : (int)e;
 }
 
-int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq, int Hkv,
-                   int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool mfma_part, KTime tm) {
-  if (n_items == 0) return 0;
-  dim3 grid(n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
+int launch_combine(int dtype, const CombineArgs& args, const TokenMeta* meta, int Hq, int Hkv, int D,
+                   const float* part_o, const float* part_ml, int part_stride_rows, void* out, hipStream_t s,
+                   bool mfma_part, KTime tm) {
+  if (args.n_items == 0) return 0;
+  dim3 grid(args.n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
 #define CB(T, DD)                                                                                            \
   if (mfma_part)                                                                                             \
-    hipExtLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, items, meta, Hq, Hkv, part_o,   \
-                       part_ml, part_stride_rows, (T*)out);                                                  \
+    hipExtLaunchKernelGGL((combine_kernel<T, DD, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args,   \
+                          meta, Hq, Hkv, part_o, part_ml, part_stride_rows, (T*)out);                         \
   else                                                                                                       \
-    hipExtLaunchKernelGGL((combine_kernel<T, DD, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, items, meta, Hq, Hkv, part_o,  \
-                       part_ml, part_stride_rows, (T*)out)
+    hipExtLaunchKernelGGL((combine_kernel<T, DD, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args,  \
+                          meta, Hq, Hkv, part_o, part_ml, part_stride_rows, (T*)out)
   if (dtype == 0) { if (D == 64) CB(float, 64); else CB(float, 128); }
   else { if (D == 64) CB(bf16_t, 64); else CB(bf16_t, 128); }
 #undef CB

@@ -80,6 +80,12 @@ struct CombineItem {
   int32_t rank0, n_rank;
   int32_t part0, n_part;  // partial slots part0 .. part0 + n_part - 1
 };
+// By-value plan of one combine launch.
+constexpr int kCombMaxItems = 128;
+struct CombineArgs {
+  int32_t n_items, pad0, pad1, pad2;
+  CombineItem item[kCombMaxItems];
+};
 
 // By-value arguments of one fused decode launch (up to kMaxDecodeSeqs sequences).
 constexpr int kMaxDecodeSeqs = 64;
@@ -146,8 +152,8 @@ int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, in
 
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
 // accumulator order of the MFMA prefill kernel.
-int launch_combine(int dtype, const CombineItem* items, int n_items, const TokenMeta* meta, int Hq,
-                   int Hkv, int D, const float* part_o, const float* part_ml, int part_stride_rows, void* out,
-                   hipStream_t s, bool mfma_part = false, KTime tm = {});
+int launch_combine(int dtype, const CombineArgs& args, const TokenMeta* meta, int Hq, int Hkv, int D,
+                   const float* part_o, const float* part_ml, int part_stride_rows, void* out, hipStream_t s,
+                   bool mfma_part = false, KTime tm = {});
 
 }  // namespace fcg
