@@ -322,3 +322,15 @@ def test_decode_split_edges(hq, hkv, d, dtype):
     lengths = [58, 61, 124, 125, 197, 252]       # contexts 61, 64, 127, 128, 200, 255 after 3 fresh tokens
     w = synth.custom(shape, 11, lengths, [[i] for i in range(len(lengths))], n_fresh=3, n_decode=3)
     run_pipeline(w, [0], 3, list(range(w.n_seqs)))
+
+
+@pytest.mark.gpu
+def test_many_sequences_split_over_launches():
+    """130 sequences: the prefill row blocks fill two attention launches (128 row blocks
+    each at most) and decode runs in three launch groups (64 sequences each at most)."""
+    from paper_2606_13097_amd import synth
+    shape = synth.Shape(1, 32, 8, 128, 1e6, "bf16")
+    n = 130
+    lengths = [40 + 7 * (i % 9) for i in range(n)]
+    w = synth.custom(shape, 13, lengths, [[i] for i in range(n)], n_fresh=2, n_decode=2)
+    run_pipeline(w, [0], 2, [0, 63, 64, 127, 128, 129])
