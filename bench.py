@@ -103,8 +103,8 @@ def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
         reps += 1
     graft_bytes = 2 * tw.grafted_tokens * 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes * n_layers_graft * reps
     # patch-attention sample: the 64 patch tokens at n_layers_attn layers
-    flops = 0
-    t_att = 0.0
+    flops = dec_bytes = 0
+    t_att = t_dec = 0.0
     for layer in range(n_layers_attn):
         items = [(int(d), int(tw.lib_src_pos0[g]), synth.lib_segment(tw, int(g), layer, "k"),
                   synth.lib_segment(tw, int(g), layer, "v")) for g, d in zip(tw.graft_seg, tw.graft_dst)]
@@ -119,6 +119,18 @@ def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
         oatt.attend(qe, pos, K, V, wr)
         t_att += time.perf_counter() - t0
         flops += 4 * sh.n_q_heads * sh.head_dim * int((pos + 1).sum())
+        # decode sample: the first n_dec decode steps (append, then one query row per head)
+        n_dec = min(16, tw.n_decode)
+        dq = synth.decode_tokens(tw, 0, layer, "q", range(n_dec))
+        dk = synth.decode_tokens(tw, 0, layer, "k", range(n_dec))
+        dv = synth.decode_tokens(tw, 0, layer, "v", range(n_dec))
+        for step in range(n_dec):
+            p = int(np.flatnonzero(wr)[-1]) + 1
+            t0 = time.perf_counter()
+            ograft.place_fresh(K, V, wr, [p], dk[step][None], dv[step][None], winv, sh.dtype)
+            oatt.attend_row(ograft.encode_fresh(dq[step][None], [p], winv, sh.dtype)[0], p, K, V, wr)
+            t_dec += time.perf_counter() - t0
+            dec_bytes += (p + 1) * 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes
     return {
         "value": round(graft_bytes / t_graft / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
         "sample": f"graft of one task's {len(tw.graft_seg)} segments ({tw.grafted_tokens} tokens) at "
@@ -127,6 +139,9 @@ def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
         "patch_attn": {"value": round(flops / t_att / 1e12, 6), "unit": "TFLOP/s", "cores": blas_threads,
                        "sample": f"64 patch tokens x {sh.n_q_heads} heads at {n_layers_attn} layers, "
                                  f"{flops / 1e9:.2f} GFLOP in {t_att:.2f} s (NumPy float64 + BLAS)"},
+        "decode": {"value": round(dec_bytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": blas_threads,
+                   "sample": f"first {n_dec} decode steps at {n_layers_attn} layers, {dec_bytes / 1e6:.1f} MB of "
+                             f"K/V in {t_dec:.3f} s (NumPy float64)"},
     }
 
 
