@@ -125,6 +125,16 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
 /* Forget everything written in seq (all layers) and return its pages. */
 fcg_status fcg_cache_reset(fcg_cache* cache, int32_t seq);
 
+/* Cache-patching (Sec. 4.2, Eq. 6; the patch step of Alg. 1): keep only the
+ * prefix [0, pos) of seq in every layer, so that the span after it can be
+ * regenerated over the reused prefix states (fcg_patch_prefill of new tokens
+ * at positions pos.., then fcg_decode).  Metadata only: no device work, the
+ * stale states past pos are never read.  Pages holding no kept position
+ * return to the pool.  pos = 0 empties the sequence; pos = max_tokens keeps
+ * everything.  Errors: EINVAL (null cache), ERANGE (seq outside [0, n_seqs),
+ * pos outside [0, max_tokens]). */
+fcg_status fcg_cache_truncate(fcg_cache* cache, int32_t seq, int32_t pos);
+
 /* Host copy of the layout of seq: page_table [ceil(max_tokens / page_size)]
  * physical page or -1 (paged caches only; may be NULL), *seq_len = 1 + the
  * highest written position of layer (0 if none; may be NULL), written

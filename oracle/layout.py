@@ -19,7 +19,8 @@ Page assignment (a reading: the paper has no paged cache; any injective map is
 valid, this one is fixed so layouts compare bit for bit): within one call,
 the logical pages that are touched and not yet mapped are mapped in ascending
 ``(sequence, logical page)`` order, each to the lowest-numbered free physical
-page.  ``reset`` returns a sequence's pages to the free pool.
+page.  ``reset`` returns a sequence's pages to the free pool; ``truncate``
+(cache-patching keeps a prefix) returns the pages past the kept prefix.
 
 Validation (checked in this order; the first failing class is reported):
 
@@ -208,3 +209,23 @@ class Layout:
             for lp in np.flatnonzero(self.page_table[seq] >= 0):
                 heapq.heappush(self._free, int(self.page_table[seq, lp]))
             self.page_table[seq] = -1
+
+    def truncate(self, seq: int, pos: int) -> None:
+        """Keep only the prefix [0, pos) of a sequence, in every layer.
+
+        Cache-patching reuses the KV states of the preserved prefix and
+        regenerates the span after it (Sec. 4.2, Eq. 6; the patch step of
+        Alg. 1): the positions from the error span on are forgotten, and the
+        pages that hold no kept position return to the pool.
+        """
+        if not (0 <= seq < self.n_seqs):
+            raise FcgError(ERANGE, f"seq {seq}")
+        if not (0 <= pos <= self.max_tokens):
+            raise FcgError(ERANGE, f"position {pos}")
+        self.written[seq, :, pos:] = False
+        if self.page_size:
+            first = -(-pos // self.page_size)        # first logical page with no kept position
+            for lp in range(first, self.page_table.shape[1]):
+                if self.page_table[seq, lp] >= 0:
+                    heapq.heappush(self._free, int(self.page_table[seq, lp]))
+                    self.page_table[seq, lp] = -1

@@ -464,6 +464,14 @@ fcg_status fcg_cache_reset(fcg_cache* c, int32_t seq) {
   return FCG_OK;
 }
 
+fcg_status fcg_cache_truncate(fcg_cache* c, int32_t seq, int32_t pos) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
+  if (pos < 0 || pos > c->max_tokens) return fail(FCG_ERANGE, "position out of range");
+  c->plan.truncate(seq, pos);  // page-table rows: as for fcg_cache_reset
+  return FCG_OK;
+}
+
 fcg_status fcg_cache_export_layout(const fcg_cache* c, int32_t seq, int32_t layer, int32_t* page_table,
                                    int32_t* seq_len, uint8_t* written) {
   if (!c) return fail(FCG_EINVAL, "null cache");

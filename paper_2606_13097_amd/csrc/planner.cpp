@@ -196,4 +196,28 @@ void Planner::reset(int32_t seq) {
   }
 }
 
+void Planner::truncate(int32_t seq, int32_t pos) {
+  for (int32_t l = 0; l < L_; ++l) {
+    uint64_t* b = bits(seq, l);
+    for (int32_t wi = 0; wi < W_; ++wi) {
+      const int32_t lo = wi * 64;
+      if (lo >= pos) b[wi] = 0;
+      else if (lo + 64 > pos) b[wi] &= (1ull << (pos - lo)) - 1;
+    }
+    int32_t cnt = 0, len = 0;
+    for (int32_t wi = 0; wi < W_; ++wi)
+      if (b[wi]) {
+        cnt += __builtin_popcountll(b[wi]);
+        len = wi * 64 + 64 - __builtin_clzll(b[wi]);
+      }
+    cnt_[idx(seq, l)] = cnt;
+    len_[idx(seq, l)] = len;
+  }
+  if (P_)
+    for (int32_t lp = (pos + P_ - 1) / P_; lp < NLP_; ++lp) {
+      int32_t& e = page_table_[(size_t)seq * NLP_ + lp];
+      if (e >= 0) { free_.insert(e); e = -1; }
+    }
+}
+
 }  // namespace fcg

@@ -48,6 +48,7 @@ class Planner {
   void mark_all_layers(int32_t seq, int32_t dst, int32_t len);
   void mark(int32_t seq, int32_t layer, int32_t pos);
   void reset(int32_t seq);
+  void truncate(int32_t seq, int32_t pos);  // keep [0, pos) in every layer; caller checked the range
 
   // Queries.
   bool written(int32_t seq, int32_t layer, int32_t pos) const;

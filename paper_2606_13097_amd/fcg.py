@@ -32,7 +32,7 @@ FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE,
 # every symbol include/fcg.h declares
 EXPORTS = [
     "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
-    "fcg_cache_create", "fcg_cache_reset", "fcg_cache_export_layout", "fcg_cache_device_ptrs",
+    "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
     "fcg_cache_timing", "fcg_cache_timing_read",
 ]
@@ -70,6 +70,7 @@ def _load():
         "fcg_lib_destroy": [P],
         "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
         "fcg_cache_reset": [P, I32],
+        "fcg_cache_truncate": [P, I32, I32],
         "fcg_cache_export_layout": [P, I32, I32, P, PI32, P],
         "fcg_cache_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
         "fcg_cache_destroy": [P],
@@ -211,6 +212,11 @@ def fcg_cache_create(desc: ModelDesc, n_seqs: int, max_tokens: int, page_size: i
 
 def fcg_cache_reset(cache: Cache, seq: int) -> None:
     _check(_L.fcg_cache_reset(cache.h, int(seq)))
+
+
+def fcg_cache_truncate(cache: Cache, seq: int, pos: int) -> None:
+    """Keep positions [0, pos) of ``seq`` in every layer (cache-patching reuses that prefix)."""
+    _check(_L.fcg_cache_truncate(cache.h, int(seq), int(pos)))
 
 
 def fcg_cache_export_layout(cache: Cache, seq: int, layer: int):

@@ -9,8 +9,9 @@ import pytest
 import torch
 
 from gpuutil import (check_attn, check_keys, oracle_items, oracle_run, read_cache, say, storage_np, to_device)
-from oracle import graft as ograft, numerics, rope
+from oracle import graft as ograft, numerics, rope, task
 from oracle.layout import Layout
+from paper_2606_13097_amd import synth
 
 pytestmark = pytest.mark.gpu
 
@@ -334,3 +335,92 @@ def test_many_sequences_split_over_launches():
     lengths = [40 + 7 * (i % 9) for i in range(n)]
     w = synth.custom(shape, 13, lengths, [[i] for i in range(n)], n_fresh=2, n_decode=2)
     run_pipeline(w, [0], 2, [0, 63, 64, 127, 128, 129])
+
+
+def _tokens(w, tag, layer, item, rows):
+    sh = w.shape
+    q = tag.endswith("q")
+    return synth.tensor_values(w.seed, tag, layer, item, np.asarray(rows), sh.n_q_heads if q else sh.n_kv_heads,
+                               sh.head_dim, w.q_scale if q else w.kv_scale, sh.dtype, w.outlier_rate)
+
+
+@pytest.mark.gpu
+@pytest.mark.parametrize("dtype,page", [("bf16", 0), ("bf16", 16), ("f32", 16)])
+def test_cache_patching_cut_regenerate_decode(dtype, page):
+    """Cache-patching (Sec. 4.2, Eq. 6): after graft -> prefill -> two decode steps,
+    each sequence is cut back to an error position -- inside its grafted context on
+    a page boundary, inside its fresh span, at its full length (nothing cut), at 0
+    (nothing kept) -- a new span is prefilled from there in one call and two more
+    decode steps follow.  Outputs, layout (freed pages taken again) and cache
+    contents match the oracle's patch step run on the oracle's own first pass."""
+    from paper_2606_13097_amd import fcg, runner
+    shape = synth.Shape(2, 32, 8, 128, 1e6, "bf16") if dtype == "bf16" else synth.Shape(2, 4, 2, 64, 1e4, "f32")
+    w = synth.custom(shape, 17, [90, 130, 200, 64], [[0, 1], [2], [3, 1], [2, 0]], n_fresh=5, n_decode=2,
+                     page_size=page)
+    keep = [96, 203, 201, 0]               # contexts 220, 200, 194, 290; 5 fresh tokens, 2 decoded
+    n_new = [37, 9, 1, 70]
+    layers = [0, 1]
+    sh = w.shape
+    say(f"[gpu] cache patching {dtype} page={page} keep={keep} new={n_new}")
+    setup = runner.GpuSetup(w)
+    try:
+        setup.graft()
+        for layer in layers:
+            q, k, v = setup.fresh_inputs(layer)
+            setup.prefill(layer, q, k, v, torch.empty_like(q))
+        for layer in layers:
+            dq, dk, dv = setup.decode_inputs(layer, 2)
+            for t in range(2):
+                setup.decode(layer, dq[t], dk[t], dv[t], torch.empty_like(dq[t]))
+        torch.cuda.synchronize()
+        for s, e in enumerate(keep):
+            fcg.fcg_cache_truncate(setup.cache, s, e)
+        seqs = np.concatenate([np.full(n, s, np.int32) for s, n in enumerate(n_new)])
+        pos = np.concatenate([np.arange(e, e + n, dtype=np.int32) for e, n in zip(keep, n_new)])
+        outs = {}
+        for layer in layers:
+            q, k, v = (to_device(np.concatenate([_tokens(w, "fresh_" + x, layer, 100 + s, np.arange(n))
+                                                 for s, n in enumerate(n_new)]), dtype) for x in "qkv")
+            out = torch.empty_like(q)
+            fcg.fcg_patch_prefill(setup.cache, layer, seqs, pos, q, k, v, out)
+            outs[("prefill", layer)] = out
+        for layer in layers:
+            for t in range(2):
+                q, k, v = (to_device(np.stack([_tokens(w, "dec_" + x, layer, 100 + s, [t])[0]
+                                               for s in range(w.n_seqs)]), dtype) for x in "qkv")
+                out = torch.empty_like(q)
+                p = fcg.fcg_decode(setup.cache, layer, np.arange(w.n_seqs), q, k, v, out)
+                assert list(p) == [e + n + t for e, n in zip(keep, n_new)]
+                outs[("decode", layer, t)] = out
+        torch.cuda.synchronize()
+        say("[gpu]   patch done")
+        ora = _oracle_layout(w, 2, layers)
+        for s, e in enumerate(keep):
+            ora.truncate(s, e)
+        for layer in layers:
+            ora.append(layer, seqs, pos)
+        for layer in layers:
+            for _ in range(2):
+                ora.decode(layer, list(range(w.n_seqs)))
+        _compare_layout(setup.cache, ora, w, layers)
+        for layer in layers:
+            for s, (e, n) in enumerate(zip(keep, n_new)):
+                state = oracle_run(w, s, layer, 2)
+                rows = np.arange(n)
+                ref = task.patch_layer(state, sh.n_q_heads, sh.head_dim, sh.rope_theta, dtype, e,
+                                       np.arange(e, e + n), *(_tokens(w, "fresh_" + x, layer, 100 + s, rows)
+                                                              for x in "qkv"),
+                                       *([_tokens(w, "dec_" + x, layer, 100 + s, [t])[0] for t in range(2)]
+                                         for x in "qkv"))
+                got = storage_np(outs[("prefill", layer)][torch.from_numpy(np.flatnonzero(seqs == s)).cuda()])
+                check_attn(got, ref["prefill"], dtype, f"patch prefill seq {s} layer {layer}")
+                for t in range(2):
+                    check_attn(storage_np(outs[("decode", layer, t)][s]), ref["decode"][t], dtype,
+                               f"patch decode seq {s} layer {layer} step {t}")
+                wpos = np.flatnonzero(ref["written"])
+                gk, gv = read_cache(setup.cache, w, layer, s, wpos)
+                np.testing.assert_array_equal(numerics.decode(gv, dtype), ref["V"][wpos])
+                check_keys(gk, ref["K"][wpos], dtype, f"patched keys seq {s} layer {layer}")
+        say("[gpu]   patch parity ok")
+    finally:
+        setup.close()

@@ -155,3 +155,39 @@ def test_needle_through_graft(dtype):
     q_enc = graft.encode_fresh(fq[-1:], [p_q], w, dtype)[0]
     o_bad = attention.attend_row(q_enc, p_q, K_bad, out["V"], out["written"])
     assert np.all(o_bad < 0.5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("keep", [0, 17, 30, 50, 53, 57, 58])
+def test_patch_equals_a_fresh_run_on_the_kept_prefix(dtype, keep):
+    """Cache-patching (Sec. 4.2, Eq. 6): cutting a finished run back to ``keep`` and
+    prefilling a new span there gives what a run built from scratch on the kept
+    prefix gives, whether the cut falls in the grafted context (on or off a segment
+    boundary), in the fresh span, among the decoded tokens, at 0 or past the end."""
+    D, Hq, Hkv, theta = 64, 4, 2, 1e4
+    items, fq, fk, fv = _task_inputs(21, D, Hq, Hkv, dtype)
+    rng = np.random.default_rng(22)
+    enc = lambda a: numerics.encode(a, dtype)
+    dq, dk, dv = (enc(rng.standard_normal((2, h, D))) for h in (Hq, Hkv, Hkv))
+    full = task.run_layer(Hq, Hkv, D, theta, dtype, 200, items, np.arange(50, 56), fq, fk, fv,
+                          list(dq), list(dk), list(dv))
+    m = 9
+    cq, ck, cv = (enc(rng.standard_normal((m, h, D))) for h in (Hq, Hkv, Hkv))
+    eq, ek, ev = (enc(rng.standard_normal((2, h, D))) for h in (Hq, Hkv, Hkv))
+    cot = np.arange(keep, keep + m)
+    got = task.patch_layer(full, Hq, D, theta, dtype, keep, cot, cq, ck, cv, list(eq), list(ek), list(ev))
+    # from scratch: graft only the kept part of each segment; kept fresh and decoded
+    # tokens (positions 50..57, encoded alike) become fresh tokens before the new span
+    cut = [(d, s, k[:keep - d], v[:keep - d]) for d, s, k, v in items if d < keep]
+    tq, tk, tv = np.concatenate([fq, dq]), np.concatenate([fk, dk]), np.concatenate([fv, dv])
+    n_old = max(0, keep - 50)
+    ref = task.run_layer(Hq, Hkv, D, theta, dtype, 200, cut, np.concatenate([np.arange(50, 50 + n_old), cot]),
+                         np.concatenate([tq[:n_old], cq]), np.concatenate([tk[:n_old], ck]),
+                         np.concatenate([tv[:n_old], cv]), list(eq), list(ek), list(ev))
+    np.testing.assert_allclose(got["prefill"], ref["prefill"][n_old:], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(got["decode"], ref["decode"], rtol=0, atol=1e-12)
+    np.testing.assert_array_equal(got["written"], ref["written"])
+    np.testing.assert_array_equal(got["K"][ref["written"]], ref["K"][ref["written"]])
+    np.testing.assert_array_equal(got["V"][ref["written"]], ref["V"][ref["written"]])
+    # the input state is left as it was
+    assert full["written"][:58].all() and not full["written"][58:].any()

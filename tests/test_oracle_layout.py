@@ -146,3 +146,76 @@ def test_random_plans_against_enumeration(data):
         # exactly the touched logical pages are mapped, and they use pages 0..k-1
         want = sum(len({p // page for p in occupied[s]}) for s in (0, 1))
         assert len(mapped) == want and sorted(mapped.tolist()) == list(range(want))
+
+
+def test_truncate_by_hand():
+    # page size 4; seq 0 grafted at 0..4 (pages 0, 1), seq 1 at 8..12 (logical pages 2, 3)
+    L = _lay(page_size=4, n_pages=8)
+    L.graft([0, 1], [1, 1], [0, 8])
+    assert L.page_table[0].tolist()[:2] == [0, 1] and L.page_table[1].tolist()[2:4] == [2, 3]
+    # keep [0, 3) of seq 0: positions 3, 4 are forgotten in every layer; page 1
+    # (positions 4..7) holds nothing kept and is freed, page 0 stays
+    L.truncate(0, 3)
+    assert not L.written[0, :, 3:].any() and L.written[0, :, :3].all()
+    assert L.page_table[0].tolist()[:2] == [0, -1]
+    assert L.seq_len(0, 0) == 3
+    # the freed page is the lowest free one and is taken first
+    L.graft([0], [0], [4])
+    assert L.page_table[0, 1] == 1
+    # decode after a truncation appends at the cut
+    L.truncate(0, 3)
+    assert L.decode(1, [0]) == [3]
+    assert L.written[0, 1, 3] and not L.written[0, 0, 3]
+    # keeping everything changes nothing; keeping nothing frees every page of the sequence
+    before = L.written.copy()
+    L.truncate(1, L.max_tokens)
+    np.testing.assert_array_equal(L.written, before)
+    L.truncate(1, 0)
+    assert not L.written[1].any() and (L.page_table[1] < 0).all()
+    for bad in ((-1, 0), (2, 0), (0, -1), (0, L.max_tokens + 1)):
+        with pytest.raises(FcgError) as e:
+            L.truncate(*bad)
+        assert e.value.code == ERANGE
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_truncate_against_enumeration(data):
+    """Grafts and truncations on a random plan, checked against explicit
+    position sets: after truncate(s, p) the written set of s is what it was,
+    cut at p, in every layer, and a logical page stays mapped iff it was
+    mapped and holds a position below p."""
+    seg_len = data.draw(st.lists(st.integers(1, 9), min_size=1, max_size=4))
+    src = [0] * len(seg_len)
+    page = data.draw(st.sampled_from([0, 4, 16]))
+    L = Layout(2, 2, 64, page, 64, seg_len, src)
+    occupied = {0: set(), 1: set()}
+    mapped = {0: set(), 1: set()}
+    for _ in range(data.draw(st.integers(1, 8))):
+        seq = data.draw(st.integers(0, 1))
+        if data.draw(st.booleans()):
+            seg = data.draw(st.integers(0, len(seg_len) - 1))
+            dst = data.draw(st.integers(0, 64 - seg_len[seg]))
+            span = set(range(dst, dst + seg_len[seg]))
+            try:
+                L.graft([seq], [seg], [dst])
+                assert not (span & occupied[seq])
+                occupied[seq] |= span
+                if page:
+                    mapped[seq] |= {p // page for p in span}
+            except FcgError as e:
+                assert span & occupied[seq] and e.code == EOVERLAP
+        else:
+            cut = data.draw(st.integers(0, 64))
+            L.truncate(seq, cut)
+            occupied[seq] = {p for p in occupied[seq] if p < cut}
+            if page:
+                mapped[seq] = {lp for lp in mapped[seq] if lp * page < cut}
+        for s in (0, 1):
+            for layer in range(2):
+                assert set(np.flatnonzero(L.written[s, layer]).tolist()) == occupied[s]
+            if page:
+                assert set(np.flatnonzero(L.page_table[s] >= 0).tolist()) == mapped[s]
+    if page:
+        pages = L.page_table[L.page_table >= 0].tolist()
+        assert len(set(pages)) == len(pages)                       # injective

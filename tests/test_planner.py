@@ -56,7 +56,7 @@ def test_append_decode_reset_match_oracle(data):
     n_pages = data.draw(st.integers(1, 12))
     _, cache, ora = _pair(n_layers, n_seqs, max_tokens, page, n_pages, [], [])
     for _ in range(data.draw(st.integers(1, 12))):
-        op = data.draw(st.sampled_from(["append", "append", "decode", "reset"]))
+        op = data.draw(st.sampled_from(["append", "append", "decode", "reset", "truncate"]))
         layer = data.draw(st.integers(-1, n_layers))
         if op == "append":
             n = data.draw(st.integers(0, 6))
@@ -71,9 +71,13 @@ def test_append_decode_reset_match_oracle(data):
                                lambda: ora.decode(layer, seqs))
             if ro is not None:
                 assert list(rc) == list(ro)
-        else:
+        elif op == "reset":
             s = data.draw(st.integers(-1, n_seqs))
             _run_both(lambda: fcg.fcg_cache_reset(cache, s), lambda: ora.reset(s))
+        else:
+            s = data.draw(st.integers(-1, n_seqs))
+            p = data.draw(st.integers(-1, max_tokens + 1))
+            _run_both(lambda: fcg.fcg_cache_truncate(cache, s, p), lambda: ora.truncate(s, p))
     _compare(cache, ora, n_seqs, n_layers)
 
 
@@ -120,6 +124,10 @@ def test_graft_plans_match_oracle(data):
         if data.draw(st.booleans()):
             s = data.draw(st.integers(0, n_seqs - 1))
             _run_both(lambda: fcg.fcg_cache_reset(cache, s), lambda: ora.reset(s))
+        if data.draw(st.booleans()):
+            s = data.draw(st.integers(0, n_seqs - 1))
+            p = data.draw(st.integers(0, max_tokens))
+            _run_both(lambda: fcg.fcg_cache_truncate(cache, s, p), lambda: ora.truncate(s, p))
     _compare(cache, ora, n_seqs, n_layers)
 
 
