@@ -12,7 +12,10 @@ come from HBM, not from the last-level cache.
 Prints ONE JSON line.  ``value`` is the graft throughput in GB/s (algorithmic
 bytes: every grafted K and V element read once and written once, divided by
 the measured graft time); the patch-attention TFLOP/s and the decode GB/s are
-reported beside it, each with its roofline.
+reported beside it, each with its roofline.  After the timed steps, each task
+is also patched (cache-patching): its cache is cut in the middle of the
+generated program, a CoT prompt as long as the patch prompt is prefilled at the
+cut, and up to 128 fill-in tokens are decoded; the ``patch`` figures time that.
 """
 from __future__ import annotations
 
@@ -28,6 +31,7 @@ sys.path.insert(0, ROOT)
 METRIC = "graft GB/s + patch-attn TFLOP/s (frac of MI355X peak), 7B GQA, 4K grafted ctx"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, published
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+FIM_MAX_TOKENS = 128           # length limit of the regenerated span (App. C hyperparameters)
 
 
 def parse():
@@ -164,7 +168,11 @@ def main():
     sh = w.shape
     n_tasks = args.steps + args.warmup
     task_ws = [synth.workload(args.workload, seed=args.seed, n_decode=nd, task=t) for t in range(n_tasks)]
-    w.max_tokens = max(t.max_tokens for t in task_ws)
+    # cache-patching after each step: cut in the middle of the generated program,
+    # prefill a CoT prompt as long as the patch prompt, decode the FIM span
+    n_fim = min(FIM_MAX_TOKENS, args.decode_steps if args.decode_steps is not None else task_ws[0].n_decode)
+    n_cot = max(int((t.fresh_seq == 0).sum()) for t in task_ws)
+    w.max_tokens = max(t.max_tokens for t in task_ws) + 64 * (-(-(n_cot + n_fim) // 64))
     log(f"bench: building the {w.name} segment library ({len(w.lib_lengths)} segments, "
         f"{int(w.lib_lengths.sum()) * sh.token_bytes / 1e9:.1f} GB)")
     t0 = time.time()
@@ -209,8 +217,33 @@ def main():
         e3 = ev()
         return e0, e1, e2, e3
 
+    def patch_plan(tw):
+        """Cut points and the CoT tokens' (sequence, position): each sequence is cut
+        in the middle of its generated program and its CoT prompt follows the cut."""
+        cut = np.array([tw.seq_len_after_prefill(s) + tw.n_decode // 2 for s in range(w.n_seqs)], np.int32)
+        return cut, tw.fresh_seq, (cut[tw.fresh_seq] + tw.fresh_row).astype(np.int32)
+
+    plans = {id(tw): patch_plan(tw) for tw in task_ws}
+
+    def run_patch(tw):
+        cut, cseq, cpos = plans[id(tw)]
+        e0 = ev()
+        for s in range(w.n_seqs):
+            fcg.fcg_cache_truncate(cache, s, int(cut[s]))
+        for l in range(sh.n_layers):
+            q, k, v, o = fresh_p[l]
+            fcg.fcg_patch_prefill(cache, l, cseq, cpos, q, k, v, o, sp)
+        e1 = ev()
+        for t in range(n_fim):
+            for l in range(sh.n_layers):
+                dq, dk, dv = dec_p[t][l]
+                fcg.fcg_decode(cache, l, all_seqs, dq, dk, dv, out_dp, sp)
+        e2 = ev()
+        return e0, e1, e2
+
     for i in range(args.warmup):
         run_task(task_ws[args.steps + i])
+        run_patch(task_ws[args.steps + i])
     torch.cuda.synchronize()
     for kind in range(5):
         fcg.fcg_cache_timing_read(cache, kind)        # drop anything recorded so far
@@ -233,6 +266,21 @@ def main():
     torch.cuda.synchronize()
     fcg.fcg_cache_timing(cache, False)
     kt = {k: fcg.fcg_cache_timing_read(cache, k) for k in range(5)}
+    # cache-patching after each of the K steps: once as a caller runs it, once with
+    # kernel timing on for the patch calls only
+    log("bench: timing cache-patching")
+    pmarks = []
+    for i in range(args.steps):
+        run_task(task_ws[i])
+        pmarks.append((task_ws[i], run_patch(task_ws[i])))
+    torch.cuda.synchronize()
+    for i in range(args.steps):
+        run_task(task_ws[i])
+        fcg.fcg_cache_timing(cache, True)
+        run_patch(task_ws[i])
+        fcg.fcg_cache_timing(cache, False)
+    torch.cuda.synchronize()
+    pkt = {k: fcg.fcg_cache_timing_read(cache, k) for k in range(5)}
 
     g_bytes = g_ms = p_flops = p_bytes = p_ms = d_bytes = d_ms = 0.0
     n_dec_calls = 0
@@ -251,6 +299,18 @@ def main():
         d_bytes += sum((ctx + t + 1) * kvb for t in range(tw.n_decode)) * sh.n_layers
         n_dec_calls += tw.n_decode * sh.n_layers
     K = args.steps
+    pp_ms = pd_ms = pp_flops = pp_bytes = pd_bytes = 0.0
+    for tw, (e0, e1, e2) in pmarks:
+        cut, cseq, cpos = plans[id(tw)]
+        pp_ms += e0.elapsed_time(e1)
+        pd_ms += e1.elapsed_time(e2)
+        pp_flops += 4 * sh.n_q_heads * sh.head_dim * float((cpos.astype(np.int64) + 1).sum()) * sh.n_layers
+        qo = 2 * len(cpos) * sh.n_q_heads * sh.head_dim * sh.elem_bytes
+        pp_bytes += (int(cpos[cseq == 0].max()) + 1) * kvb * sh.n_layers + qo * sh.n_layers
+        end = int(cpos[cseq == 0].max()) + 1
+        pd_bytes += sum((end + t + 1) * kvb for t in range(n_fim)) * sh.n_layers
+    (_, _), (pna, pa_kms), (npp, pp_kms), (npd, pd_kms), (npda, pda_kms) = (pkt[k] for k in range(5))
+    assert pna == npp == K * sh.n_layers and npd == npda == K * sh.n_layers * n_fim, pkt
     (ng, g_kms), (na, a_kms), (npf, p_kms), (nd_, d_kms), (nda, da_kms) = kt[0], kt[1], kt[2], kt[3], kt[4]
     assert ng == K and na == K * sh.n_layers and npf == K * sh.n_layers and nd_ == n_dec_calls, kt
     assert nda == n_dec_calls, kt
@@ -296,6 +356,16 @@ def main():
                    "with_merge_gbs": round(decode_gbs, 2),
                    "with_merge_us_per_layer_step": round(d_kms * 1e3 / n_dec_calls, 2),
                    "call_us_per_layer_step": round(d_ms * 1e3 / n_dec_calls, 2)},
+        "patch": {"cut": "middle of the generated program", "cot_tokens": n_cot, "fim_tokens": n_fim,
+                  "ms_per_patch": round((pp_ms + pd_ms) / K, 3),
+                  "cut_and_cot_prefill_call_us_per_layer": round(pp_ms * 1e3 / (K * sh.n_layers), 2),
+                  "cot_attn_kernel_us_per_layer": round(pa_kms * 1e3 / (K * sh.n_layers), 2),
+                  "cot_attn_tflops": round(pp_flops / (pa_kms / 1e3) / 1e12, 3),
+                  "cot_attn_gbs": round(pp_bytes / (pa_kms / 1e3) / 1e9, 2),
+                  "fim_decode_call_us_per_layer_step": round(pd_ms * 1e3 / (K * sh.n_layers * n_fim), 2),
+                  "fim_decode_kernel_us_per_layer_step": round(pda_kms * 1e3 / npda, 2),
+                  "fim_decode_kernel_gbs": round(pd_bytes / (pda_kms / 1e3) / 1e9, 2),
+                  "fim_decode_kernel_frac": round(pd_bytes / (pda_kms / 1e3) / 1e9 / HBM_PEAK_GBS, 4)},
         "graft_kernel_us": round(g_kms * 1e3 / K, 2),
         "graft_call_us": round(g_ms * 1e3 / K, 2),
         "wall_s_timed": round(t_wall, 3),
