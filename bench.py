@@ -321,7 +321,7 @@ def main():
     p_intensity = p_flops / p_bytes
     p_bound = "mfma" if p_intensity * HBM_PEAK_GBS / 1e3 >= BF16_PEAK_TFLOPS else "hbm"
     prefill_tflops = p_flops / (p_kms / 1e3) / 1e12            # append + attention + merge kernels
-    decode_gbs = d_bytes / (d_kms / 1e3) / 1e9                 # decode + merge kernels
+    decode_gbs = d_bytes / (d_kms / 1e3) / 1e9                 # every kernel of the decode calls
     decode_attn_gbs = d_bytes / (da_kms / 1e3) / 1e9           # decode attention kernel
     ms_per_step = (g_ms + p_ms + d_ms) / K
     res = {

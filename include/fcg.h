@@ -193,8 +193,9 @@ fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int
  *   FCG_TIME_GRAFT        the graft kernel of fcg_graft
  *   FCG_TIME_PREFILL_ATTN the attention kernel of fcg_patch_prefill
  *   FCG_TIME_PREFILL      all kernels of fcg_patch_prefill (append, attention, merge)
- *   FCG_TIME_DECODE       all kernels of fcg_decode (attention, merge)
- *   FCG_TIME_DECODE_ATTN  the attention kernel of fcg_decode
+ *   FCG_TIME_DECODE       all kernels of fcg_decode (one per group of 64 sequences)
+ *   FCG_TIME_DECODE_ATTN  the attention kernels of fcg_decode (the same kernels: the
+ *                         split merge runs inside them)
  * Plan uploads and host work are outside the intervals.  fcg_cache_timing_read
  * waits for the recorded events, returns the number of intervals and their
  * summed duration in milliseconds for one kind (ERANGE for another value),

@@ -182,6 +182,7 @@ struct fcg_cache {
   size_t part_bytes = 0;
   float* dpart = nullptr;     // decode split partials
   size_t dpart_bytes = 0;
+  int32_t* d_count = nullptr; // decode merge arrival counters [kMaxDecodeSeqs][Hkv] (kCountStride apart), zero between launches
   // kernel timing (fcg_cache_timing): recorded (start, end) event pairs per kind
   bool timing = false;
   std::vector<std::pair<hipEvent_t, hipEvent_t>> spans[5];
@@ -440,6 +441,10 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
       const size_t pt = (size_t)n_seqs * c->plan.n_logical_pages() * sizeof(int32_t);
       ok = hipMalloc((void**)&c->d_page_table, pt) == hipSuccess && hipMemset(c->d_page_table, 0xFF, pt) == hipSuccess;
     }
+    if (ok) {
+      const size_t nc = (size_t)kMaxDecodeSeqs * desc->n_kv_heads * kCountStride * sizeof(int32_t);
+      ok = hipMalloc((void**)&c->d_count, nc) == hipSuccess && hipMemset(c->d_count, 0, nc) == hipSuccess;
+    }
     if (!ok) {
       fcg_cache_destroy(c);
       return fail(FCG_ENOMEM, "cache does not fit in device memory");
@@ -536,6 +541,7 @@ fcg_status fcg_cache_destroy(fcg_cache* c) {
     if (c->qws) hipFree(c->qws);
     if (c->part) hipFree(c->part);
     if (c->dpart) hipFree(c->dpart);
+    if (c->d_count) hipFree(c->d_count);
     for (auto& v : c->spans)
       for (auto& sp : v) {
         if (sp.first) hipEventDestroy(sp.first);
@@ -738,10 +744,9 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   return c->ring.retire(off, blob.bytes.size(), s);
 }
 
-// One decode launch per group of up to kMaxDecodeSeqs sequences, then one
-// merge launch for the sequences split over several blocks; both take their
-// plan by value, so a decode step uploads nothing (new pages aside).  Split
-// size: blocks fill the chip twice over in one wave.
+// One decode launch per group of up to kMaxDecodeSeqs sequences; the launch
+// merges the splits of each sequence itself and takes its plan by value, so a
+// decode step uploads nothing (new pages aside).
 fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
                       const void* q, const void* k, const void* v, void* out,
                       const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
@@ -753,10 +758,13 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     total += pos[i] + 1;
     pmax = std::max(pmax, pos[i]);
   }
-  // split length: the smallest (from 64 keys up) whose blocks fit two per
-  // compute unit, so the grid runs in one wave; at most 256 splits per
-  // sequence (the merge table)
-  const int64_t target_blocks = 512;
+  // split length: the smallest (from 64 keys up) whose blocks fit in one
+  // wave of the grid -- one block per compute unit when few (sequence, kv
+  // head) pairs are split many ways, so that the merge in each pair's last
+  // block stays short; two per compute unit for larger batches, where the
+  // loads of a second block hide latency -- rounded up to whole 64-key
+  // chunks; at most 256 splits per sequence
+  const int64_t target_blocks = (int64_t)n * d.n_kv_heads < 128 ? 256 : 512;
   int64_t sk = std::max<int64_t>(64, (total * d.n_kv_heads + target_blocks - 1) / target_blocks);
   sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);
   for (;;) {
@@ -765,6 +773,7 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     if (blocks * d.n_kv_heads <= target_blocks || blocks <= n) break;
     sk += (sk + 31) / 32;  // about 3% longer
   }
+  sk = (sk + 63) / 64 * 64;
   // partial slots: one per split of every multi-split sequence of a launch group
   int max_slots = 0;
   for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {
@@ -801,23 +810,16 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
       a.max_split = std::max(a.max_split, ns);
     }
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
-    // timing: the decode kernel's dispatch opens both intervals and closes
-    // its own; the merge kernel (if launched) closes the call's
-    const bool merge = a.max_split > 1;
+    // timing: one kernel, both intervals
     const hipEvent_t e0 = timing_event(c), e1 = timing_event(c);
-    const hipEvent_t e2 = merge ? timing_event(c) : e1;
     int rc = launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv, layer,
-                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, s, KTime{e0, e1});
+                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, c->d_count, s,
+                           KTime{e0, e1});
     if (rc) return hip_fail((hipError_t)rc, "decode launch");
-    if (merge) {
-      rc = launch_decode_combine(d.dtype, a, d.n_q_heads, d.n_kv_heads, d.head_dim, part_o, part_ml,
-                                 (char*)out + qoff, s, KTime{nullptr, e2});
-      if (rc) return hip_fail((hipError_t)rc, "decode combine launch");
-    }
     time_open(c, FCG_TIME_DECODE_ATTN, e0);
     time_close(c, FCG_TIME_DECODE_ATTN, e1);
     time_open(c, FCG_TIME_DECODE, e0);
-    time_close(c, FCG_TIME_DECODE, e2);
+    time_close(c, FCG_TIME_DECODE, e1);
   }
   return FCG_OK;
 }

@@ -76,6 +76,34 @@ __device__ __forceinline__ void st8_nt(void* p, uint32_t lo, uint32_t hi) {
 }
 __device__ __forceinline__ void st16(void* p, const uint4& v) { *reinterpret_cast<uint4*>(p) = v; }
 
+// Device-coherent accesses for data that one block writes and another block
+// of the same launch reads (the XCDs' L2 caches are not coherent with each
+// other): relaxed device-scope atomic stores, and buffer loads with the
+// device-scope cache policy.  Buffer loads past num_records return zeros.
+__device__ __forceinline__ void st_dev(float* p, float x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_dev_u32(uint32_t* p, uint32_t x) {
+  __hip_atomic_store(p, x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+constexpr int kBufWord3 = 0x00020000;  // raw 32-bit buffer (no format conversion)
+constexpr int kPolicyDevice = 16;      // sc1: coherent at device scope
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, kBufWord3);
+}
+__device__ __forceinline__ u32x4_t ld16_dev(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, kPolicyDevice);
+}
+__device__ __forceinline__ u32x2_t ld8_dev(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b64(r, off, 0, kPolicyDevice);
+}
+// s_waitcnt vmcnt(0): every vector memory access of this wave has completed
+__device__ __forceinline__ void wait_vm0() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  asm volatile("" ::: "memory");
+}
+
 // cos and sin of pos * w for the rotary pair with float64 frequency w: the
 // angle is the float64 product and the float64 cos/sin are rounded to fp32.
 __device__ __forceinline__ void rope_cs(double pos, double w, float* c, float* s) {

@@ -22,10 +22,11 @@
 //     other block touches that slot;
 //   - the block merges its key slots through LDS; a single-split sequence
 //     writes its output, otherwise the block stores a partial (max, sum,
-//     unnormalised output) that the decode merge kernel combines.  The merge
-//     is a separate launch on purpose: merging in the last-arriving block
-//     needs a device-scope release/acquire per block, which on gfx950 writes
-//     back and invalidates the XCD's whole L2.
+//     unnormalised output) with device-coherent stores, waits for them to
+//     complete and counts itself in the (sequence, kv head) counter; the
+//     block that arrives last combines every split's partial (read with
+//     device-coherent loads, so no L2 write-back or invalidation is needed)
+//     and writes the output, then sets the counter back to zero.
 #include "fcg_device.hpp"
 #include "kernels.hpp"
 
@@ -52,12 +53,19 @@ __device__ __forceinline__ float lanes_sum(float x) {
   return x;
 }
 
+template <int W>  // sum over the lanes of a wave that are W, 2W, ... apart
+__device__ __forceinline__ float lanes_sum_stride(float x) {
+#pragma unroll
+  for (int o = W; o < 64; o *= 2) x += __shfl_xor(x, o);
+  return x;
+}
+
 template <typename T, int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* __restrict__ q,
                                                      const T* __restrict__ k, const T* __restrict__ v, CacheView cv,
                                                      int layer, const double* __restrict__ inv_freq,
                                                      T* __restrict__ out, float* __restrict__ part_o,
-                                                     float* __restrict__ part_ml) {
+                                                     float* __restrict__ part_ml, int* __restrict__ count) {
   constexpr int VEC = Store<T>::VEC;
   constexpr int NV = (D / VEC > 16) ? (D / VEC) / 16 : 1;
   constexpr int DPL = VEC * NV;    // dims per lane
@@ -71,8 +79,12 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   constexpr int NW = DPL / 2;          // packed pairs per lane
   __shared__ float s_cos[HALF], s_sin[HALF];
   __shared__ float s_m[SLOTS][G], s_l[SLOTS][G];
-  __shared__ float s_o[SLOTS][JB][D];
+  // slot outputs [SLOTS][JB][D]; in the cross-split merge, the split
+  // lanes' outputs of a round of heads
+  constexpr int NBUF = SLOTS * JB * D;
+  __shared__ float s_buf[NBUF];
   __shared__ float s_L[G];
+  __shared__ int s_last;
 
   const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
   const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
@@ -83,7 +95,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   // every kernel argument in one batch of scalar loads before the first branch
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
                "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
-               "s"(out), "s"(part_o), "s"(part_ml));
+               "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
   if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
   if (split >= nsplit) return;  // padding split of a shorter sequence
 
@@ -300,7 +312,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       const float f = (M == -INFINITY || mx[j] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mx[j] - M);
 #pragma unroll
       for (int e = 0; e < DPL; e += 4)
-        *reinterpret_cast<float4*>(&s_o[slot][jj][d0 + e]) =
+        *reinterpret_cast<float4*>(&s_buf[(slot * JB + jj) * D + d0 + e]) =
             make_float4(o[j][e] * f, o[j][e + 1] * f, o[j][e + 2] * f, o[j][e + 3] * f);
     }
     if (jb == 0 && t < G) {  // block sums of the heads
@@ -314,77 +326,176 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
       s_L[t] = L;
     }
     __syncthreads();
-    for (int idx = t; idx < JB * D; idx += 256) {
-      const int jj = idx / D, d = idx % D, j = jb + jj;
-      float acc = 0.f;
+    // two adjacent output dims per lane
+    for (int idx = t; idx < JB * D / 2; idx += 256) {
+      const int jj = idx / (D / 2), d = 2 * (idx % (D / 2)), j = jb + jj;
+      float a0 = 0.f, a1 = 0.f;
 #pragma unroll 8
-      for (int s2 = 0; s2 < SLOTS; ++s2) acc += s_o[s2][jj][d];
+      for (int s2 = 0; s2 < SLOTS; ++s2) {
+        const float2 x = *reinterpret_cast<const float2*>(&s_buf[(s2 * JB + jj) * D + d]);
+        a0 += x.x;
+        a1 += x.y;
+      }
       const float L = s_L[j];
       if (nsplit == 1) {
-        Store<T>::store1(out + ((int64_t)i * Hq + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
+        T* dst = out + ((int64_t)i * Hq + hk * G + j) * D + d;
+        Store<T>::store1(dst, L > 0.f ? a0 / L : 0.f);
+        Store<T>::store1(dst + 1, L > 0.f ? a1 / L : 0.f);
       } else {
-        // partial slot of this split in the merge layout [slot][Hkv][G][D] (+ [slot][Hkv][G][2])
-        part_o[(prow + j) * D + d] = acc;
+        // partial slot of this split in the merge layout [slot][Hkv][G][D]
+        // (+ [slot][Hkv][G][2]); bf16 rows for bf16 storage
+        if constexpr (BF)
+          st_dev_u32(reinterpret_cast<uint32_t*>(part_o) + ((prow + j) * D + d) / 2, pack_bf16x2(a0, a1));
+        else {
+          st_dev(&part_o[(prow + j) * D + d], a0);
+          st_dev(&part_o[(prow + j) * D + d + 1], a1);
+        }
         if (d == 0) {
           float M = -INFINITY;
 #pragma unroll
           for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][j]);
-          part_ml[(prow + j) * 2 + 0] = M;
-          part_ml[(prow + j) * 2 + 1] = L;
+          st_dev(&part_ml[(prow + j) * 2 + 0], M);
+          st_dev(&part_ml[(prow + j) * 2 + 1], L);
         }
+      }
+    }
+  }
+  if (nsplit == 1) return;
+
+  // ---- cross-split merge in the last block of (sequence, kv head) to finish
+  wait_vm0();        // this wave's partial stores have completed
+  __syncthreads();   // ... and every wave's
+  if (t == 0) {
+    int* c = count + (i * Hkv + hk) * kCountStride;
+    const int before = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = before == nsplit - 1;
+    if (before == nsplit - 1) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  {
+    // O = sum_s O_s 2^(M_s - M) / sum_s L_s 2^(M_s - M), M = max_s M_s, per
+    // query head.  Lane (split lane sl, 16-byte chunk dc of a row) folds the
+    // splits sl, sl + NSL, ... of its chunk into a running (max, sum, output)
+    // per head, as in the key loop; the NSL split lanes of each chunk are then
+    // merged through LDS like the key slots above.
+    constexpr int EB = BF ? 2 : 4;            // bytes per partial element
+    constexpr int EPL = 16 / EB;              // elements per 16-byte chunk
+    constexpr int NDC = D / EPL, NSL = 256 / NDC;
+    static_assert(NSL <= SLOTS, "split lanes use the slot tables");
+    constexpr int PF = G >= 8 ? 16 / G : 32 / G;  // splits per lane per batch of loads
+    constexpr int NMLV = G >= 2 ? G / 2 : 1;      // 16-byte loads of a split's (max, sum) pairs
+    constexpr int JR = (SLOTS * JB) / NSL < G ? (SLOTS * JB) / NSL : G;  // heads per LDS round
+    static_assert(JR >= 1 && NSL * JR * D <= NBUF, "merge rounds");
+    const int dc = t % NDC, sl = t / NDC;
+    const int64_t hg = (int64_t)Hkv * G;      // rows per partial slot
+    const int64_t row0 = (int64_t)slot0 * hg + (int64_t)hk * G;
+    const uint32_t rows_all = (uint32_t)(args.split0[args.n] * hg);
+    const __amdgpu_buffer_rsrc_t ro = buf_rsrc(part_o, rows_all * D * EB);
+    const __amdgpu_buffer_rsrc_t rml = buf_rsrc(part_ml, rows_all * 8u);
+    float acc[G][EPL], lm[G], ll[G];
+#pragma unroll
+    for (int j = 0; j < G; ++j) {
+      lm[j] = -INFINITY;
+      ll[j] = 0.f;
+#pragma unroll
+      for (int e = 0; e < EPL; ++e) acc[j][e] = 0.f;
+    }
+    for (int sb = 0; sb < nsplit; sb += NSL * PF) {
+      u32x4_t rv[PF][G], mv[PF][NMLV];
+#pragma unroll
+      for (int p = 0; p < PF; ++p) {
+        const int sp = min(sb + sl + p * NSL, nsplit - 1);
+        const int64_t r = row0 + (int64_t)sp * hg;
+#pragma unroll
+        for (int h = 0; h < NMLV; ++h) {
+          if constexpr (G >= 2) {
+            mv[p][h] = ld16_dev(rml, (uint32_t)((r + 2 * h) * 8));
+          } else {
+            const u32x2_t x = ld8_dev(rml, (uint32_t)(r * 8));
+            mv[p][h] = u32x4_t{x.x, x.y, 0u, 0u};
+          }
+        }
+#pragma unroll
+        for (int j = 0; j < G; ++j) rv[p][j] = ld16_dev(ro, (uint32_t)(((r + j) * D + dc * EPL) * EB));
+      }
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        auto mval = [&](int p) { return __uint_as_float(j % 2 ? mv[p][j / 2].z : mv[p][j / 2].x); };
+        auto lval = [&](int p) { return __uint_as_float(j % 2 ? mv[p][j / 2].w : mv[p][j / 2].y); };
+        float bm = -INFINITY;
+#pragma unroll
+        for (int p = 0; p < PF; ++p)
+          if (sb + sl + p * NSL < nsplit) bm = fmaxf(bm, mval(p));
+        const float mn = fmaxf(lm[j], bm);
+        if (mn == -INFINITY) continue;
+        const float f = __builtin_amdgcn_exp2f(lm[j] - mn);  // 0 while nothing was folded
+        ll[j] *= f;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) acc[j][e] *= f;
+#pragma unroll
+        for (int p = 0; p < PF; ++p) {
+          if (sb + sl + p * NSL >= nsplit) continue;
+          const float wgt = __builtin_amdgcn_exp2f(mval(p) - mn);
+          ll[j] = fmaf(lval(p), wgt, ll[j]);
+          float x[EPL];
+          if constexpr (BF) {
+            Store<T>::unpack(make_uint4(rv[p][j].x, rv[p][j].y, rv[p][j].z, rv[p][j].w), x);
+          } else {
+            x[0] = __uint_as_float(rv[p][j].x);
+            x[1] = __uint_as_float(rv[p][j].y);
+            x[2] = __uint_as_float(rv[p][j].z);
+            x[3] = __uint_as_float(rv[p][j].w);
+          }
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) acc[j][e] = fmaf(x[e], wgt, acc[j][e]);
+        }
+        lm[j] = mn;
+      }
+    }
+    // merge the split lanes: per head, M over the lanes, each lane's output
+    // and sum weighted by 2^(m - M)
+    if (dc == 0) {
+#pragma unroll
+      for (int j = 0; j < G; ++j) { s_m[sl][j] = lm[j]; s_l[sl][j] = ll[j]; }
+    }
+#pragma unroll
+    for (int jr = 0; jr < G; jr += JR) {
+      if (jr) __syncthreads();  // the previous round's sums are read
+#pragma unroll
+      for (int jj = 0; jj < JR; ++jj)
+#pragma unroll
+        for (int e = 0; e < EPL; e += 4)
+          *reinterpret_cast<float4*>(&s_buf[(sl * JR + jj) * D + dc * EPL + e]) =
+              make_float4(acc[jr + jj][e], acc[jr + jj][e + 1], acc[jr + jj][e + 2], acc[jr + jj][e + 3]);
+      __syncthreads();
+      for (int idx = t; idx < JR * D / 2; idx += 256) {
+        const int jj = idx / (D / 2), d = 2 * (idx % (D / 2)), j = jr + jj;
+        float M = -INFINITY;
+#pragma unroll
+        for (int s2 = 0; s2 < NSL; ++s2) M = fmaxf(M, s_m[s2][j]);
+        float L = 0.f, o0 = 0.f, o1 = 0.f;
+        if (M != -INFINITY) {
+#pragma unroll 8
+          for (int s2 = 0; s2 < NSL; ++s2) {
+            const float ms = s_m[s2][j];
+            const float wgt = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
+            const float2 x = *reinterpret_cast<const float2*>(&s_buf[(s2 * JR + jj) * D + d]);
+            L = fmaf(s_l[s2][j], wgt, L);
+            o0 = fmaf(x.x, wgt, o0);
+            o1 = fmaf(x.y, wgt, o1);
+          }
+        }
+        T* dst = out + ((int64_t)i * Hq + hk * G + j) * D + d;
+        Store<T>::store1(dst, L > 0.f ? o0 / L : 0.f);
+        Store<T>::store1(dst + 1, L > 0.f ? o1 / L : 0.f);
       }
     }
   }
 }
 
-// Merge of the decode partials: block (sequence, kv head, query head of the
-// group), one lane per output dim.  O = sum_s O_s 2^(M_s - M) / sum_s L_s
-// 2^(M_s - M) with M = max_s M_s.  The first 64 splits' partial rows are
-// loaded together with the (M_s, L_s) pairs.
-template <typename T, int D, int G>
-__global__ void __launch_bounds__(D) decode_combine_kernel(DecodeArgs args, const float* __restrict__ part_o,
-                                                           const float* __restrict__ part_ml, int Hkv,
-                                                           T* __restrict__ out) {
-  constexpr int P0 = 64;
-  __shared__ float s_m[256], s_l[256];
-  const int i = blockIdx.x, hk = blockIdx.y, j = blockIdx.z;
-  const int slot0 = args.split0[i];
-  const int ns = args.split0[i + 1] - slot0;
-  asm volatile("" ::"s"(slot0), "s"(ns), "s"(part_o), "s"(part_ml), "s"(out), "s"(Hkv));
-  if (ns <= 1) return;  // written by the decode kernel
-  const int d = threadIdx.x;
-  auto row = [&](int s) { return ((int64_t)(slot0 + s) * Hkv + hk) * G + j; };
-  float ov[P0];
-#pragma unroll
-  for (int u = 0; u < P0; ++u) ov[u] = part_o[row(min(u, ns - 1)) * D + d];
-  for (int s = d; s < ns; s += D) {
-    s_m[s] = part_ml[row(s) * 2 + 0];
-    s_l[s] = part_ml[row(s) * 2 + 1];
-  }
-  __syncthreads();
-  float M = -INFINITY;
-#pragma unroll 8
-  for (int s = 0; s < ns; ++s) M = fmaxf(M, s_m[s]);
-  float L = 0.f, acc = 0.f;
-#pragma unroll
-  for (int u = 0; u < P0; ++u) {
-    const float m = s_m[min(u, ns - 1)];
-    const float w = (u < ns && m != -INFINITY) ? exp2f(m - M) : 0.f;
-    L = fmaf(s_l[min(u, ns - 1)], w, L);
-    acc = fmaf(ov[u], w, acc);
-  }
-#pragma unroll 8
-  for (int s = P0; s < ns; ++s) {
-    const float m = s_m[s];
-    const float w = m != -INFINITY ? exp2f(m - M) : 0.f;
-    L = fmaf(s_l[s], w, L);
-    acc = fmaf(part_o[row(s) * D + d], w, acc);
-  }
-  Store<T>::store1(out + ((int64_t)i * Hkv * G + hk * G + j) * D + d, L > 0.f ? acc / L : 0.f);
-}
-
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml, int* count,
                   hipStream_t s, KTime tm) {
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
@@ -392,10 +503,10 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
 #define DK(T, DD, GG)                                                                                       \
   if (cv.page_size)                                                                                         \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,          \
-                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml);             \
+                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml, count);             \
   else                                                                                                      \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,         \
-                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml)
+                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml, count)
 #define DKG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
     case 1: DK(T, DD, 1); break;                                                                            \
@@ -409,30 +520,6 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
   else { if (cv.head_dim == 64) { DKG(bf16_t, 64) } else { DKG(bf16_t, 128) } }
 #undef DKG
 #undef DK
-  hipError_t e = hipGetLastError();
-  return e == hipSuccess ? 0 : (int)e;
-}
-
-int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
-                          const float* part_ml, void* out, hipStream_t s, KTime tm) {
-  if (args.n == 0 || args.max_split <= 1) return 0;
-  const int g = Hq / Hkv;
-  dim3 grid(args.n, Hkv, g);
-#define DC(T, DD, GG)                                                                                       \
-  hipExtLaunchKernelGGL((decode_combine_kernel<T, DD, GG>), grid, dim3(DD), 0, s, tm.start, tm.stop, 0, args, part_o, part_ml, Hkv, (T*)out)
-#define DCG(T, DD)                                                                                          \
-  switch (g) {                                                                                              \
-    case 1: DC(T, DD, 1); break;                                                                            \
-    case 2: DC(T, DD, 2); break;                                                                            \
-    case 4: DC(T, DD, 4); break;                                                                            \
-    case 8: DC(T, DD, 8); break;                                                                            \
-    case 16: DC(T, DD, 16); break;                                                                          \
-    default: return -1;                                                                                     \
-  }
-  if (dtype == 0) { if (D == 64) { DCG(float, 64) } else { DCG(float, 128) } }
-  else { if (D == 64) { DCG(bf16_t, 64) } else { DCG(bf16_t, 128) } }
-#undef DCG
-#undef DC
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

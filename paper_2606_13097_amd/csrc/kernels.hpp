@@ -141,14 +141,14 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 // cache.  q, k, v, out: [n][H][D] rows in the order of args.seq.  Grid
 // (max_split, n, Hkv).  Splits of multi-split sequences leave partials in
 // part_o [slot][Hkv][g][D] and part_ml [slot][Hkv][g][2], slot = split0[i] +
-// split, merged by launch_decode_combine.
+// split; the last block of each (sequence, kv head) to finish merges them.
+// count: [kMaxDecodeSeqs][Hkv] arrival counters kCountStride ints apart (one
+// per 128-byte line: atomics on one line serialise), zero before the launch
+// and zero again after it.
+constexpr int kCountStride = 32;
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml, int* count,
                   hipStream_t s, KTime tm = {});
-
-// Merge the decode partials of the multi-split sequences of args into out.
-int launch_decode_combine(int dtype, const DecodeArgs& args, int Hq, int Hkv, int D, const float* part_o,
-                          const float* part_ml, void* out, hipStream_t s, KTime tm = {});
 
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
 // accumulator order of the MFMA prefill kernel.

@@ -326,6 +326,17 @@ def test_decode_split_edges(hq, hkv, d, dtype):
 
 
 @pytest.mark.gpu
+@pytest.mark.parametrize("hq,d,dtype", [(16, 128, "bf16"), (8, 128, "bf16"), (16, 128, "f32"), (4, 64, "f32")])
+def test_decode_merge_of_many_splits(hq, d, dtype):
+    """One kv head and a ~3K-token context: 47 splits of 64 keys, so the last block's
+    merge of the splits takes several rounds of loads (large query groups) and several
+    rounds of LDS sums (16 query heads)."""
+    shape = synth.Shape(1, hq, 1, d, 1e4, dtype)
+    w = synth.custom(shape, 19, [2990], [[0]], n_fresh=3, n_decode=3)
+    run_pipeline(w, [0], 3, [0])
+
+
+@pytest.mark.gpu
 def test_many_sequences_split_over_launches():
     """130 sequences: the prefill row blocks fill two attention launches (128 row blocks
     each at most) and decode runs in three launch groups (64 sequences each at most)."""
