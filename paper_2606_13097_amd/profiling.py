@@ -59,8 +59,9 @@ def _per_dispatch(path: str, kernel: str, counter: str):
 
 
 def traffic(args) -> dict:
-    f = _per_dispatch(args.fetch, args.kernel, "FETCH_SIZE")[args.skip:]
-    w = _per_dispatch(args.write, args.kernel, "WRITE_SIZE")[args.skip:]
+    end = args.skip + args.take if args.take else None
+    f = _per_dispatch(args.fetch, args.kernel, "FETCH_SIZE")[args.skip:end]
+    w = _per_dispatch(args.write, args.kernel, "WRITE_SIZE")[args.skip:end]
     cf = max(v for v in _per_dispatch(args.copy_fetch, args.copy_kernel, "FETCH_SIZE"))
     cw = max(v for v in _per_dispatch(args.copy_write, args.copy_kernel, "WRITE_SIZE"))
     ff = args.copy_bytes / (cf * 1024.0)
@@ -85,7 +86,8 @@ def main(argv=None):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
     t.add_argument("--copy-kernel", default="copyBuffer")
     t.add_argument("--copy-bytes", type=float, default=float(1 << 30))
-    t.add_argument("--skip", type=int, default=0)
+    t.add_argument("--skip", type=int, default=0, help="dispatches to leave out first (warm-up)")
+    t.add_argument("--take", type=int, default=0, help="dispatches to average after those (0: all)")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         sys.stdout.write(stats_markdown(a.csv, a.title, a.command))
