@@ -812,9 +812,14 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
     // timing: one kernel, both intervals
     const hipEvent_t e0 = timing_event(c), e1 = timing_event(c);
-    int rc = launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv, layer,
-                           c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, c->d_count, s,
-                           KTime{e0, e1});
+    // bf16: matrix-core kernel; fp32: the vector-ALU kernel
+    int rc = d.dtype == FCG_BF16
+                 ? launch_decode_mfma(a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv,
+                                      layer, c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml,
+                                      c->d_count, s, KTime{e0, e1})
+                 : launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv,
+                                 layer, c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, c->d_count, s,
+                                 KTime{e0, e1});
     if (rc) return hip_fail((hipError_t)rc, "decode launch");
     time_open(c, FCG_TIME_DECODE_ATTN, e0);
     time_close(c, FCG_TIME_DECODE_ATTN, e1);

@@ -27,8 +27,7 @@
 //     block that arrives last combines every split's partial (read with
 //     device-coherent loads, so no L2 write-back or invalidation is needed)
 //     and writes the output, then sets the counter back to zero.
-#include "fcg_device.hpp"
-#include "kernels.hpp"
+#include "decode_common.hpp"
 
 namespace fcg {
 
@@ -299,7 +298,6 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     for (int j = 0; j < G; ++j) { s_m[slot][j] = mx[j]; s_l[slot][j] = sm[j]; }
   }
   __syncthreads();
-  const int64_t prow = ((int64_t)(slot0 + split) * Hkv + hk) * G;
 #pragma unroll
   for (int jb = 0; jb < G; jb += JB) {
     if (jb) __syncthreads();  // the previous round's sums are read
@@ -336,162 +334,19 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
         a0 += x.x;
         a1 += x.y;
       }
-      const float L = s_L[j];
-      if (nsplit == 1) {
-        T* dst = out + ((int64_t)i * Hq + hk * G + j) * D + d;
-        Store<T>::store1(dst, L > 0.f ? a0 / L : 0.f);
-        Store<T>::store1(dst + 1, L > 0.f ? a1 / L : 0.f);
-      } else {
-        // partial slot of this split in the merge layout [slot][Hkv][G][D]
-        // (+ [slot][Hkv][G][2]); bf16 rows for bf16 storage
-        if constexpr (BF)
-          st_dev_u32(reinterpret_cast<uint32_t*>(part_o) + ((prow + j) * D + d) / 2, pack_bf16x2(a0, a1));
-        else {
-          st_dev(&part_o[(prow + j) * D + d], a0);
-          st_dev(&part_o[(prow + j) * D + d + 1], a1);
-        }
-        if (d == 0) {
-          float M = -INFINITY;
+      float M = -INFINITY;
+      if (d == 0 && nsplit > 1) {
 #pragma unroll
-          for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][j]);
-          st_dev(&part_ml[(prow + j) * 2 + 0], M);
-          st_dev(&part_ml[(prow + j) * 2 + 1], L);
-        }
+        for (int s2 = 0; s2 < SLOTS; ++s2) M = fmaxf(M, s_m[s2][j]);
       }
+      emit_pair<T, D>(nsplit, part_row(slot0 + split, Hkv, hk, G, j), out + ((int64_t)i * Hq + hk * G + j) * D,
+                      part_o, part_ml, d, a0, a1, M, s_L[j]);
     }
   }
   if (nsplit == 1) return;
-
-  // ---- cross-split merge in the last block of (sequence, kv head) to finish
-  wait_vm0();        // this wave's partial stores have completed
-  __syncthreads();   // ... and every wave's
-  if (t == 0) {
-    int* c = count + (i * Hkv + hk) * kCountStride;
-    const int before = __hip_atomic_fetch_add(c, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = before == nsplit - 1;
-    if (before == nsplit - 1) __hip_atomic_store(c, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-  __syncthreads();
-  if (!s_last) return;
-  {
-    // O = sum_s O_s 2^(M_s - M) / sum_s L_s 2^(M_s - M), M = max_s M_s, per
-    // query head.  Lane (split lane sl, 16-byte chunk dc of a row) folds the
-    // splits sl, sl + NSL, ... of its chunk into a running (max, sum, output)
-    // per head, as in the key loop; the NSL split lanes of each chunk are then
-    // merged through LDS like the key slots above.
-    constexpr int EB = BF ? 2 : 4;            // bytes per partial element
-    constexpr int EPL = 16 / EB;              // elements per 16-byte chunk
-    constexpr int NDC = D / EPL, NSL = 256 / NDC;
-    static_assert(NSL <= SLOTS, "split lanes use the slot tables");
-    constexpr int PF = G >= 8 ? 16 / G : 32 / G;  // splits per lane per batch of loads
-    constexpr int NMLV = G >= 2 ? G / 2 : 1;      // 16-byte loads of a split's (max, sum) pairs
-    constexpr int JR = (SLOTS * JB) / NSL < G ? (SLOTS * JB) / NSL : G;  // heads per LDS round
-    static_assert(JR >= 1 && NSL * JR * D <= NBUF, "merge rounds");
-    const int dc = t % NDC, sl = t / NDC;
-    const int64_t hg = (int64_t)Hkv * G;      // rows per partial slot
-    const int64_t row0 = (int64_t)slot0 * hg + (int64_t)hk * G;
-    const uint32_t rows_all = (uint32_t)(args.split0[args.n] * hg);
-    const __amdgpu_buffer_rsrc_t ro = buf_rsrc(part_o, rows_all * D * EB);
-    const __amdgpu_buffer_rsrc_t rml = buf_rsrc(part_ml, rows_all * 8u);
-    float acc[G][EPL], lm[G], ll[G];
-#pragma unroll
-    for (int j = 0; j < G; ++j) {
-      lm[j] = -INFINITY;
-      ll[j] = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[j][e] = 0.f;
-    }
-    for (int sb = 0; sb < nsplit; sb += NSL * PF) {
-      u32x4_t rv[PF][G], mv[PF][NMLV];
-#pragma unroll
-      for (int p = 0; p < PF; ++p) {
-        const int sp = min(sb + sl + p * NSL, nsplit - 1);
-        const int64_t r = row0 + (int64_t)sp * hg;
-#pragma unroll
-        for (int h = 0; h < NMLV; ++h) {
-          if constexpr (G >= 2) {
-            mv[p][h] = ld16_dev(rml, (uint32_t)((r + 2 * h) * 8));
-          } else {
-            const u32x2_t x = ld8_dev(rml, (uint32_t)(r * 8));
-            mv[p][h] = u32x4_t{x.x, x.y, 0u, 0u};
-          }
-        }
-#pragma unroll
-        for (int j = 0; j < G; ++j) rv[p][j] = ld16_dev(ro, (uint32_t)(((r + j) * D + dc * EPL) * EB));
-      }
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        auto mval = [&](int p) { return __uint_as_float(j % 2 ? mv[p][j / 2].z : mv[p][j / 2].x); };
-        auto lval = [&](int p) { return __uint_as_float(j % 2 ? mv[p][j / 2].w : mv[p][j / 2].y); };
-        float bm = -INFINITY;
-#pragma unroll
-        for (int p = 0; p < PF; ++p)
-          if (sb + sl + p * NSL < nsplit) bm = fmaxf(bm, mval(p));
-        const float mn = fmaxf(lm[j], bm);
-        if (mn == -INFINITY) continue;
-        const float f = __builtin_amdgcn_exp2f(lm[j] - mn);  // 0 while nothing was folded
-        ll[j] *= f;
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) acc[j][e] *= f;
-#pragma unroll
-        for (int p = 0; p < PF; ++p) {
-          if (sb + sl + p * NSL >= nsplit) continue;
-          const float wgt = __builtin_amdgcn_exp2f(mval(p) - mn);
-          ll[j] = fmaf(lval(p), wgt, ll[j]);
-          float x[EPL];
-          if constexpr (BF) {
-            Store<T>::unpack(make_uint4(rv[p][j].x, rv[p][j].y, rv[p][j].z, rv[p][j].w), x);
-          } else {
-            x[0] = __uint_as_float(rv[p][j].x);
-            x[1] = __uint_as_float(rv[p][j].y);
-            x[2] = __uint_as_float(rv[p][j].z);
-            x[3] = __uint_as_float(rv[p][j].w);
-          }
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[j][e] = fmaf(x[e], wgt, acc[j][e]);
-        }
-        lm[j] = mn;
-      }
-    }
-    // merge the split lanes: per head, M over the lanes, each lane's output
-    // and sum weighted by 2^(m - M)
-    if (dc == 0) {
-#pragma unroll
-      for (int j = 0; j < G; ++j) { s_m[sl][j] = lm[j]; s_l[sl][j] = ll[j]; }
-    }
-#pragma unroll
-    for (int jr = 0; jr < G; jr += JR) {
-      if (jr) __syncthreads();  // the previous round's sums are read
-#pragma unroll
-      for (int jj = 0; jj < JR; ++jj)
-#pragma unroll
-        for (int e = 0; e < EPL; e += 4)
-          *reinterpret_cast<float4*>(&s_buf[(sl * JR + jj) * D + dc * EPL + e]) =
-              make_float4(acc[jr + jj][e], acc[jr + jj][e + 1], acc[jr + jj][e + 2], acc[jr + jj][e + 3]);
-      __syncthreads();
-      for (int idx = t; idx < JR * D / 2; idx += 256) {
-        const int jj = idx / (D / 2), d = 2 * (idx % (D / 2)), j = jr + jj;
-        float M = -INFINITY;
-#pragma unroll
-        for (int s2 = 0; s2 < NSL; ++s2) M = fmaxf(M, s_m[s2][j]);
-        float L = 0.f, o0 = 0.f, o1 = 0.f;
-        if (M != -INFINITY) {
-#pragma unroll 8
-          for (int s2 = 0; s2 < NSL; ++s2) {
-            const float ms = s_m[s2][j];
-            const float wgt = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - M);
-            const float2 x = *reinterpret_cast<const float2*>(&s_buf[(s2 * JR + jj) * D + d]);
-            L = fmaf(s_l[s2][j], wgt, L);
-            o0 = fmaf(x.x, wgt, o0);
-            o1 = fmaf(x.y, wgt, o1);
-          }
-        }
-        T* dst = out + ((int64_t)i * Hq + hk * G + j) * D + d;
-        Store<T>::store1(dst, L > 0.f ? o0 / L : 0.f);
-        Store<T>::store1(dst + 1, L > 0.f ? o1 / L : 0.f);
-      }
-    }
-  }
+  static_assert(merge_lanes<T, D>() <= SLOTS, "split lanes use the slot tables");
+  merge_splits<T, D, G, NBUF>(args, i, hk, slot0, nsplit, Hkv, Hq, out, part_o, part_ml, count, s_buf, &s_m[0][0],
+                              &s_l[0][0], &s_last);
 }
 
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,

@@ -150,6 +150,12 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
                   int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml, int* count,
                   hipStream_t s, KTime tm = {});
 
+// The same step on matrix cores for bf16 caches and query groups of up to 16
+// heads (same arguments; -1 for a group size it has no instance for).
+int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
+                       int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                       int* count, hipStream_t s, KTime tm = {});
+
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
 // accumulator order of the MFMA prefill kernel.
 int launch_combine(int dtype, const CombineArgs& args, const TokenMeta* meta, int Hq, int Hkv, int D,
