@@ -759,12 +759,12 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     pmax = std::max(pmax, pos[i]);
   }
   // split length: the smallest (from 64 keys up) whose blocks fit in one
-  // wave of the grid -- one block per compute unit when few (sequence, kv
-  // head) pairs are split many ways, so that the merge in each pair's last
-  // block stays short; two per compute unit for larger batches, where the
-  // loads of a second block hide latency -- rounded up to whole 64-key
-  // chunks; at most 256 splits per sequence
-  const int64_t target_blocks = (int64_t)n * d.n_kv_heads < 128 ? 256 : 512;
+  // wave of the grid -- one block per compute unit while that leaves at most
+  // 256 keys per block (fewer partials for the merge in each (sequence, kv
+  // head)'s last block), two per compute unit for more keys (shorter key
+  // loops) -- rounded up to whole 64-key chunks; at most 256 splits per
+  // sequence
+  const int64_t target_blocks = total * d.n_kv_heads <= 256 * 256 ? 256 : 512;
   int64_t sk = std::max<int64_t>(64, (total * d.n_kv_heads + target_blocks - 1) / target_blocks);
   sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);
   for (;;) {

@@ -135,9 +135,10 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
       vv[r] = ld16(cvv + kv_offset<PAGED>(cv, layer, seq, hk, pv) + dg * 8);
     }
   };
-  uint4 kA[KS], vA[4], kB[KS], vB[4];
+  uint4 kA[KS], vA[4], kB[KS], vB[4], kC[KS], vC[4];
   load_tile(w, kA, vA);
   load_tile(w + 4, kB, vB);
+  load_tile(w + 8, kC, vC);
   if (t < HALF) rope_cs((double)pos, wfreq, &s_cos[t], &s_sin[t]);
   __syncthreads();
 
@@ -227,13 +228,17 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
     asm volatile("" ::: "memory");  // ... and before the next tile's writes
   };
 
-  // two register sets: the tile after next is in flight while one is attended
-  for (int ti = w; ti < ntile; ti += 8) {
+  // three register sets: the wave's next two tiles are in flight while one
+  // is attended (a 192-key split is loaded entirely before the first math)
+  for (int ti = w; ti < ntile; ti += 12) {
     attend_tile(kA, vA, k0 + ti * 16, min(16, kend - k0 - ti * 16));
-    load_tile(ti + 8, kA, vA);
+    load_tile(ti + 12, kA, vA);
     if (ti + 4 >= ntile) break;
     attend_tile(kB, vB, k0 + (ti + 4) * 16, min(16, kend - k0 - (ti + 4) * 16));
-    load_tile(ti + 12, kB, vB);
+    load_tile(ti + 16, kB, vB);
+    if (ti + 8 >= ntile) break;
+    attend_tile(kC, vC, k0 + (ti + 8) * 16, min(16, kend - k0 - (ti + 8) * 16));
+    load_tile(ti + 20, kC, vC);
   }
 
   if (owns_new) __syncthreads();  // the new token is in LDS (a block-uniform branch)
