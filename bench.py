@@ -388,7 +388,7 @@ def main():
             "intensity_flop_per_byte": round(p_intensity, 1),
             "mfma_frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4),
             "hbm_frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
-        "roofline_decode": {"bound": "hbm", "kernel": "fcg decode_kernel", "achieved": round(decode_attn_gbs, 2),
+        "roofline_decode": {"bound": "hbm", "kernel": "fcg decode_mfma_kernel" if sh.dtype == "bf16" else "fcg decode_kernel", "achieved": round(decode_attn_gbs, 2),
                             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_attn_gbs / HBM_PEAK_GBS, 4),
                             "traffic": measured_traffic("decode_7b_traffic.json"),
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},

@@ -8,7 +8,7 @@
 ``traffic`` averages the kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) over its
 dispatches after the first ``--skip`` ones, and calibrates each counter by what it reads
 for a plain device copy of ``--copy-bytes`` bytes.  The JSON records the SHA-256 of the
-kernel's source file: ``bench.py`` reports the traffic only while that source is unchanged.
+kernel's source files: ``bench.py`` reports the traffic only while they are unchanged.
 """
 from __future__ import annotations
 
@@ -23,8 +23,12 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 
 
 def source_sha256(rel: str) -> str:
-    with open(os.path.join(PKG, rel), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 over the kernel's source files (``a.hip+b.hpp``: their bytes in that order)."""
+    h = hashlib.sha256()
+    for part in rel.split("+"):
+        with open(os.path.join(PKG, part), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def _short(name: str) -> str:
