@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="7b")
+    ap.add_argument("--alias-v", action="store_true",
+                    help="paged workloads: map grafted value pages onto the library (FCG_ALIAS_V)")
     ap.add_argument("--seed", type=int, default=1)
     ap.add_argument("--decode-steps", type=int, default=None, help="override the workload's decode steps")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -74,6 +76,21 @@ def copy_probe(gib: float) -> None:
     b.copy_(a)
     torch.cuda.synchronize()
     log(f"copy probe: {n * 2} bytes read, {n * 2} bytes written")
+
+
+def graft_bytes(tw, kvb, n_layers, alias_v):
+    """Algorithmic graft bytes of one task: every grafted K and V row read once and
+    written once; with value pages mapped onto the library, the values of pages a
+    segment covers entirely are neither read nor written."""
+    total = 0
+    for g, d in zip(tw.graft_seg, tw.graft_dst):
+        n, d = int(tw.lib_lengths[g]), int(d)
+        aliased = 0
+        if alias_v:
+            first = -(-d // 16)
+            aliased = max(0, (d + n) // 16 - first) * 16
+        total += n * kvb + (n - aliased) * kvb   # K rows + V rows, each read and written: 2 x half of kvb
+    return total * n_layers
 
 
 def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
@@ -176,7 +193,10 @@ def main():
     log(f"bench: building the {w.name} segment library ({len(w.lib_lengths)} segments, "
         f"{int(w.lib_lengths.sum()) * sh.token_bytes / 1e9:.1f} GB)")
     t0 = time.time()
-    setup = runner.GpuSetup(w)
+    if args.alias_v and not w.page_size:
+        print("--alias-v needs a paged workload (batched)", file=sys.stderr)
+        sys.exit(2)
+    setup = runner.GpuSetup(w, cache_flags=fcg.FCG_ALIAS_V if args.alias_v else 0)
     log(f"bench: library ready in {time.time() - t0:.1f} s")
     fresh = [setup.fresh_inputs(l) for l in range(sh.n_layers)]
     dec = [setup.decode_inputs(l) for l in range(sh.n_layers)]
@@ -289,7 +309,7 @@ def main():
         g_ms += e0.elapsed_time(e1)
         p_ms += e1.elapsed_time(e2)
         d_ms += e2.elapsed_time(e3)
-        g_bytes += 2 * tw.grafted_tokens * kvb * sh.n_layers
+        g_bytes += graft_bytes(tw, kvb, sh.n_layers, args.alias_v)
         p_flops += 4 * sh.n_q_heads * sh.head_dim * float((tw.fresh_pos.astype(np.int64) + 1).sum()) * sh.n_layers
         # HBM bytes the attention must move: the visible keys and values once, the
         # encoded queries in and the outputs out
@@ -338,10 +358,14 @@ def main():
         "dtype": sh.dtype,
         "data": "synthetic (seeded counter-hash generator; no benchmark items, no weights)",
         "config": {
-            "workload": f"{w.name}: 7B-class GQA cache, {sh.n_layers} layers, {sh.n_q_heads}/{sh.n_kv_heads} heads, "
-                        f"head_dim {sh.head_dim}, {sh.dtype}; graft 1024-token prefix + 6 of "
-                        f"{len(w.lib_lengths) - 1} library segments (U[200,800] tokens); 64 patch tokens; "
-                        f"{w.n_decode} decode steps; batch 1",
+            "workload": (f"{w.name}: 7B-class GQA cache, {sh.n_layers} layers, {sh.n_q_heads}/{sh.n_kv_heads} heads, "
+                         f"head_dim {sh.head_dim}, {sh.dtype}; graft 1024-token prefix + 6 of "
+                         f"{len(w.lib_lengths) - 1} library segments (U[200,800] tokens); 64 patch tokens; "
+                         f"{w.n_decode} decode steps; batch 1") if w.name == "7b" else
+                        (f"{w.name}: {sh.n_layers} layers, {sh.n_q_heads}/{sh.n_kv_heads} heads, head_dim "
+                         f"{sh.head_dim}, {sh.dtype}; {w.n_seqs} sequences, {len(w.lib_lengths)} library segments; "
+                         f"{len(w.fresh_pos)} patch tokens; {w.n_decode} decode steps; page size {w.page_size}"),
+            "alias_v": bool(args.alias_v),
             "grafted_tokens_mean": round(float(np.mean([t.grafted_tokens for t, _ in marks])), 1),
             "library_gb": round(int(w.lib_lengths.sum()) * sh.token_bytes / 1e9, 2),
             "distinct_task_per_step": True,

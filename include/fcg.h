@@ -78,6 +78,12 @@ typedef struct fcg_cache fcg_cache;
 
 /* flags of fcg_lib_create and fcg_cache_create */
 #define FCG_LAYOUT_ONLY 1u /* no device memory: only the index / layout is kept (planning and tests) */
+/* fcg_cache_create, paged caches only: a logical page that one grafted
+ * segment covers entirely reads its values from the library in place instead
+ * of a copy (values are position-independent; keys are still turned and
+ * copied).  The cache binds to the library of its first graft; the library
+ * must outlive the cache. */
+#define FCG_ALIAS_V 2u
 
 /* Create an empty segment library (the KV side of the two-tier code cache,
  * Sec. 4.1, Eq. 2) holding up to capacity_tokens tokens in up to max_segments
@@ -116,9 +122,11 @@ fcg_status fcg_lib_destroy(fcg_lib* lib);
  * p / 16 of a sequence is mapped on first write to the lowest-numbered free
  * page, new pages of one call in ascending (sequence, logical page) order.
  * With FCG_LAYOUT_ONLY no device memory is allocated and graft, prefill
- * and decode only validate and record the layout (planning and tests).
+ * and decode only validate and record the layout (planning and tests);
+ * FCG_ALIAS_V maps value pages onto the library (see the flag).
  * Errors: EINVAL (bad descriptor, n_seqs or max_tokens < 1, max_tokens *
- * head_dim >= 2^31, page_size not 0 or 16, unknown flags), ENOMEM, EHIP. */
+ * head_dim >= 2^31, page_size not 0 or 16, unknown flags, FCG_ALIAS_V on a
+ * contiguous cache), ENOMEM, EHIP. */
 fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t max_tokens,
                             int32_t page_size, int32_t n_pages, uint32_t flags, fcg_cache** out);
 
@@ -128,12 +136,14 @@ fcg_status fcg_cache_reset(fcg_cache* cache, int32_t seq);
 /* Cache-patching (Sec. 4.2, Eq. 6; the patch step of Alg. 1): keep only the
  * prefix [0, pos) of seq in every layer, so that the span after it can be
  * regenerated over the reused prefix states (fcg_patch_prefill of new tokens
- * at positions pos.., then fcg_decode).  Metadata only: no device work, the
- * stale states past pos are never read.  Pages holding no kept position
- * return to the pool.  pos = 0 empties the sequence; pos = max_tokens keeps
- * everything.  Errors: EINVAL (null cache), ERANGE (seq outside [0, n_seqs),
- * pos outside [0, max_tokens]). */
-fcg_status fcg_cache_truncate(fcg_cache* cache, int32_t seq, int32_t pos);
+ * at positions pos.., then fcg_decode).  The stale states past pos are never
+ * read.  Pages holding no kept position return to the pool.  Host metadata
+ * only, except with FCG_ALIAS_V when the cut splits a page whose values are
+ * read from the library: its kept rows are copied into the cache's own page
+ * on stream (new tokens will follow them).  pos = 0 empties the sequence;
+ * pos = max_tokens keeps everything.  Errors: EINVAL (null cache), ERANGE
+ * (seq outside [0, n_seqs), pos outside [0, max_tokens]), EHIP. */
+fcg_status fcg_cache_truncate(fcg_cache* cache, int32_t seq, int32_t pos, void* stream);
 
 /* Host copy of the layout of seq: page_table [ceil(max_tokens / page_size)]
  * physical page or -1 (paged caches only; may be NULL), *seq_len = 1 + the
@@ -141,6 +151,13 @@ fcg_status fcg_cache_truncate(fcg_cache* cache, int32_t seq, int32_t pos);
  * [max_tokens] bytes 1/0 per position of layer (may be NULL). */
 fcg_status fcg_cache_export_layout(const fcg_cache* cache, int32_t seq, int32_t layer,
                                    int32_t* page_table, int32_t* seq_len, uint8_t* written);
+
+/* FCG_ALIAS_V caches: v_alias [ceil(max_tokens / 16)] receives, per logical
+ * page of seq, the library token (index into the [Hkv][capacity][D] slabs)
+ * whose value row holds the page's first position, or -1 where the page holds
+ * its own values.  -1 everywhere for other caches.  Errors: EINVAL (null
+ * argument), ERANGE (seq). */
+fcg_status fcg_cache_export_v_alias(const fcg_cache* cache, int32_t seq, int32_t* v_alias);
 
 /* Device base pointers of layer's K and V region (layouts in the file header). */
 fcg_status fcg_cache_device_ptrs(const fcg_cache* cache, int32_t layer, void** k, void** v);
@@ -159,7 +176,8 @@ fcg_status fcg_cache_destroy(fcg_cache* cache);
  * Errors: ERANGE (seq, seg, span outside [0, max_tokens)), EOVERLAP (spans
  * meet each other or written positions of any layer), ENOMEM (pages), EINVAL
  * (lib and cache shapes differ, null arrays, a layout-only library with a
- * cache that has device memory). */
+ * cache that has device memory, an FCG_ALIAS_V cache bound to another
+ * library). */
 fcg_status fcg_graft(fcg_cache* cache, const fcg_lib* lib, int32_t n_items, const int32_t* seq,
                      const int32_t* seg, const int32_t* dst, void* stream);
 

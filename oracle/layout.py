@@ -61,7 +61,13 @@ class FcgError(Exception):
 
 class Layout:
     def __init__(self, n_layers: int, n_seqs: int, max_tokens: int, page_size: int,
-                 n_pages: int, seg_len: Sequence[int], seg_src_pos0: Sequence[int]):
+                 n_pages: int, seg_len: Sequence[int], seg_src_pos0: Sequence[int],
+                 alias_v: bool = False):
+        """``alias_v`` (paged only): a logical page that one grafted segment
+        covers entirely takes its values from the library in place; ``v_alias``
+        holds the library token of the page's first position (the library
+        stores segments back to back, segment g from ``sum(seg_len[:g])``),
+        -1 where the page holds its own values."""
         self.n_layers = int(n_layers)
         self.n_seqs = int(n_seqs)
         self.max_tokens = int(max_tokens)
@@ -78,6 +84,9 @@ class Layout:
         else:
             self.page_table = np.zeros((self.n_seqs, 0), dtype=np.int32)
             self._free = []
+        self.alias_v = bool(alias_v) and self.page_size > 0
+        self.v_alias = np.full(self.page_table.shape, -1, dtype=np.int32)
+        self.seg_tok0 = np.concatenate([[0], np.cumsum(self.seg_len)]).astype(np.int64)[:len(self.seg_len)]
 
     # -- queries ---------------------------------------------------------------
     def seq_len(self, seq: int, layer: int) -> int:
@@ -143,6 +152,11 @@ class Layout:
         self._map(need)
         for s, g, d in zip(seqs, segs, dsts):
             self.written[s, :, d:d + self.seg_len[g]] = True
+            if self.alias_v:
+                P = self.page_size
+                for lp in range(d // P, (d + self.seg_len[g]) // P):
+                    if lp * P >= d:    # the page lies inside the segment's span
+                        self.v_alias[s, lp] = self.seg_tok0[g] + lp * P - d
         return [(s, g, d, d - self.seg_src_pos0[g]) for s, g, d in zip(seqs, segs, dsts)]
 
     def append(self, layer: int, seqs, positions) -> None:
@@ -205,6 +219,7 @@ class Layout:
         if not (0 <= seq < self.n_seqs):
             raise FcgError(ERANGE, f"seq {seq}")
         self.written[seq] = False
+        self.v_alias[seq] = -1
         if self.page_size:
             for lp in np.flatnonzero(self.page_table[seq] >= 0):
                 heapq.heappush(self._free, int(self.page_table[seq, lp]))
@@ -225,6 +240,9 @@ class Layout:
         self.written[seq, :, pos:] = False
         if self.page_size:
             first = -(-pos // self.page_size)        # first logical page with no kept position
+            # a page split by the cut keeps its first rows but takes new
+            # tokens after them: it holds its own values from now on
+            self.v_alias[seq, pos // self.page_size:] = -1
             for lp in range(first, self.page_table.shape[1]):
                 if self.page_table[seq, lp] >= 0:
                     heapq.heappush(self._free, int(self.page_table[seq, lp]))

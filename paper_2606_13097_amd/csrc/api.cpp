@@ -182,6 +182,7 @@ struct fcg_cache {
   size_t part_bytes = 0;
   float* dpart = nullptr;     // decode split partials
   size_t dpart_bytes = 0;
+  const fcg_lib* alias_lib = nullptr;  // FCG_ALIAS_V: the library value pages map onto (bound by the first graft)
   int32_t* d_count = nullptr; // decode merge arrival counters [kMaxDecodeSeqs][Hkv] (kCountStride apart), zero between launches
   // kernel timing (fcg_cache_timing): recorded (start, end) event pairs per kind
   bool timing = false;
@@ -191,7 +192,7 @@ struct fcg_cache {
 
   fcg_cache(const fcg_model_desc& d, int32_t ns, int32_t mt, int32_t ps, int32_t np, uint32_t fl)
       : desc(d), n_seqs(ns), max_tokens(mt), page_size(ps), n_pages(np), flags(fl),
-        plan(d.n_layers, ns, mt, ps, np) {}
+        plan(d.n_layers, ns, mt, ps, np, (fl & FCG_ALIAS_V) != 0) {}
   bool layout_only() const { return flags & FCG_LAYOUT_ONLY; }
 
   CacheView view() const {
@@ -200,6 +201,9 @@ struct fcg_cache {
     c.v = v;
     c.layer_stride = layer_stride;
     c.page_table = d_page_table;
+    c.v_alias = plan.alias_v() && d_page_table ? d_page_table + plan.n_logical_pages() : nullptr;
+    c.lib_v = alias_lib ? alias_lib->v : nullptr;
+    c.lib_cap = alias_lib ? alias_lib->cap : 0;
     c.n_seqs = n_seqs;
     c.max_tokens = max_tokens;
     c.page_size = page_size;
@@ -278,6 +282,15 @@ fcg_status grow(void** p, size_t* have, size_t need, const char* what) {
 
 // After a planner check: map the new pages, and prepare the device copies of
 // the touched page-table rows (appended to the blob).
+// The device row of seq: its page row, then its value-alias row.
+size_t stage_row(const fcg_cache* c, int32_t seq, Blob* blob) {
+  const size_t nlp = c->plan.n_logical_pages();
+  std::vector<int32_t> row(2 * nlp);
+  std::memcpy(row.data(), c->plan.page_row(seq), nlp * sizeof(int32_t));
+  std::memcpy(row.data() + nlp, c->plan.alias_row(seq), nlp * sizeof(int32_t));
+  return blob->add(row.data(), row.size() * sizeof(int32_t));
+}
+
 void stage_pages(fcg_cache* c, const std::vector<std::pair<int32_t, int32_t>>& new_pages, Blob* blob,
                  std::vector<std::pair<int32_t, size_t>>* rows) {
   c->plan.map_pages(new_pages);
@@ -285,8 +298,7 @@ void stage_pages(fcg_cache* c, const std::vector<std::pair<int32_t, int32_t>>& n
   for (auto& sl : new_pages) seqs.push_back(sl.first);
   std::sort(seqs.begin(), seqs.end());
   seqs.erase(std::unique(seqs.begin(), seqs.end()), seqs.end());
-  for (int32_t s : seqs)
-    rows->push_back({s, blob->add(c->plan.page_row(s), sizeof(int32_t) * c->plan.n_logical_pages())});
+  for (int32_t s : seqs) rows->push_back({s, stage_row(c, s, blob)});
 }
 
 // Upload the blob; copy page rows into the device page table.  *dev receives
@@ -301,8 +313,8 @@ fcg_status upload(fcg_cache* c, const Blob& blob, const std::vector<std::pair<in
           "hipMemcpyAsync(plan)");
   const size_t nlp = c->plan.n_logical_pages();
   for (auto& r : rows)
-    HIP_TRY(hipMemcpyAsync(c->d_page_table + (size_t)r.first * nlp, c->ring.dev + off + r.second,
-                           nlp * sizeof(int32_t), hipMemcpyDeviceToDevice, s),
+    HIP_TRY(hipMemcpyAsync(c->d_page_table + (size_t)r.first * 2 * nlp, c->ring.dev + off + r.second,
+                           2 * nlp * sizeof(int32_t), hipMemcpyDeviceToDevice, s),
             "hipMemcpyAsync(page table)");
   *dev = c->ring.dev + off;
   *off_out = off;
@@ -427,7 +439,8 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
     return fail(FCG_EINVAL, "max_tokens * head_dim must stay below 2^31");
   if (page_size != 0 && page_size != 16) return fail(FCG_EINVAL, "page_size must be 0 (contiguous) or 16");
   if (page_size && n_pages < 1) return fail(FCG_EINVAL, "a paged cache needs n_pages >= 1");
-  if (flags & ~FCG_LAYOUT_ONLY) return fail(FCG_EINVAL, "unknown flags");
+  if (flags & ~(FCG_LAYOUT_ONLY | FCG_ALIAS_V)) return fail(FCG_EINVAL, "unknown flags");
+  if ((flags & FCG_ALIAS_V) && !page_size) return fail(FCG_EINVAL, "FCG_ALIAS_V needs a paged cache");
   fcg_cache* c = new (std::nothrow) fcg_cache(*desc, n_seqs, max_tokens, page_size, page_size ? n_pages : 0, flags);
   if (!c) return fail(FCG_ENOMEM, "host allocation");
   if (!c->layout_only()) {
@@ -438,7 +451,7 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
     const size_t bytes = (size_t)per_layer * desc->n_layers * esize(desc->dtype);
     bool ok = hipMalloc(&c->k, bytes) == hipSuccess && hipMalloc(&c->v, bytes) == hipSuccess;
     if (ok && page_size) {
-      const size_t pt = (size_t)n_seqs * c->plan.n_logical_pages() * sizeof(int32_t);
+      const size_t pt = (size_t)n_seqs * 2 * c->plan.n_logical_pages() * sizeof(int32_t);
       ok = hipMalloc((void**)&c->d_page_table, pt) == hipSuccess && hipMemset(c->d_page_table, 0xFF, pt) == hipSuccess;
     }
     if (ok) {
@@ -469,11 +482,35 @@ fcg_status fcg_cache_reset(fcg_cache* c, int32_t seq) {
   return FCG_OK;
 }
 
-fcg_status fcg_cache_truncate(fcg_cache* c, int32_t seq, int32_t pos) {
+fcg_status fcg_cache_truncate(fcg_cache* c, int32_t seq, int32_t pos, void* stream) {
   if (!c) return fail(FCG_EINVAL, "null cache");
   if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
   if (pos < 0 || pos > c->max_tokens) return fail(FCG_ERANGE, "position out of range");
-  c->plan.truncate(seq, pos);  // page-table rows: as for fcg_cache_reset
+  std::vector<Unalias> un;
+  c->plan.truncate(seq, pos, &un);  // freed page-table rows: as for fcg_cache_reset
+  if (un.empty() || c->layout_only()) return FCG_OK;
+  // a value page mapped onto the library and split by the cut: copy its kept
+  // rows into the page and upload the sequence's row without the alias
+  HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
+  hipStream_t s = (hipStream_t)stream;
+  Blob blob;
+  std::vector<std::pair<int32_t, size_t>> rows{{seq, stage_row(c, seq, &blob)}};
+  std::vector<UnaliasItem> items;
+  for (const Unalias& u : un) items.push_back(UnaliasItem{u.lib_tok, u.page, u.rows});
+  const size_t o_items = blob.add(items.data(), items.size() * sizeof(UnaliasItem));
+  char* dev;
+  size_t off;
+  if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  int rc = launch_unalias(c->desc.dtype, (const UnaliasItem*)(dev + o_items), (int)items.size(), c->alias_lib->v,
+                          c->alias_lib->cap, c->view(), c->desc.n_layers, s);
+  if (rc) return hip_fail((hipError_t)rc, "unalias launch");
+  return c->ring.retire(off, blob.bytes.size(), s);
+}
+
+fcg_status fcg_cache_export_v_alias(const fcg_cache* c, int32_t seq, int32_t* v_alias) {
+  if (!c || !v_alias) return fail(FCG_EINVAL, "null cache or output");
+  if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
+  std::memcpy(v_alias, c->plan.alias_row(seq), sizeof(int32_t) * c->plan.n_logical_pages());
   return FCG_OK;
 }
 
@@ -574,6 +611,12 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   std::string msg;
   if (fcg_status st = c->plan.check_graft(spans, &new_pages, &msg)) return fail(st, msg);
   if (n_items == 0) return FCG_OK;
+  if (c->plan.alias_v() && c->alias_lib && c->alias_lib != lib)
+    return fail(FCG_EINVAL, "a cache with FCG_ALIAS_V grafts from one library only");
+  if (c->plan.alias_v()) {
+    c->alias_lib = lib;
+    for (auto& sp : spans) c->plan.alias_pages(sp.seq, sp.dst, sp.len, lib->segs[sp.seg].tok_off);
+  }
   if (c->layout_only()) {
     c->plan.map_pages(new_pages);
     for (auto& s : spans) c->plan.mark_all_layers(s.seq, s.dst, s.len);
@@ -588,7 +631,8 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   for (auto& sp : spans) {
     const Segment& sg = lib->segs[sp.seg];
     for (int32_t j = 0; j < sp.len; j += kGraftChunk)
-      chunks.push_back(GraftChunk{sg.tok_off + j, sp.dst + j, sp.seq, sp.delta, std::min(kGraftChunk, sp.len - j), 0, 0});
+      chunks.push_back(GraftChunk{sg.tok_off + j, sp.dst + j, sp.seq, sp.delta, std::min(kGraftChunk, sp.len - j),
+                                  sp.dst, sp.dst + sp.len});
   }
   const size_t o_chunks = blob.add(chunks.data(), chunks.size() * sizeof(GraftChunk));
   char* dev;

@@ -91,7 +91,7 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
   asm volatile("" ::"s"(rb.rank0), "s"(rb.n_rank), "s"(rb.seq), "s"(rb.rmin), "s"(kend), "s"(part), "s"(meta),
                "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(Hkv),
                "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
   if (k0 >= kend) return;  // padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
@@ -124,7 +124,7 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
     return PAGED ? ck + kv_offset<true>(cv, layer, rb.seq, hk, p) : kbase + p * D;
   };
   auto vrow = [&](int p) -> const bf16_t* {
-    return PAGED ? cvv + kv_offset<true>(cv, layer, rb.seq, hk, p) : vbase + p * D;
+    return PAGED ? v_row<true, bf16_t>(cv, layer, rb.seq, hk, p) : vbase + p * D;
   };
 
   float mrow[2] = {-INFINITY, -INFINITY};

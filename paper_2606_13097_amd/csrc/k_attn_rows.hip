@@ -84,11 +84,12 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
     const int key = base + slot;
     if (key < end) {  // uniform across the LPK lanes of a key, so DPP partners are active
       const int64_t off = cache_offset(cv, layer, m.seq, hk, key) + chunk * DPL;
+      const T* vr = (cv.page_size ? v_row<true, T>(cv, layer, m.seq, hk, key) : cvv + off - chunk * DPL) + chunk * DPL;
       float kx[DPL], vx[DPL];
 #pragma unroll
       for (int nv = 0; nv < NV; ++nv) {
         Store<T>::unpack(ld16(ck + off + nv * VEC), kx + nv * VEC);
-        Store<T>::unpack(ld16(cvv + off + nv * VEC), vx + nv * VEC);
+        Store<T>::unpack(ld16(vr + nv * VEC), vx + nv * VEC);
       }
       float s[G];
 #pragma unroll

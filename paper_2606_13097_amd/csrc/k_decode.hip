@@ -95,7 +95,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
                "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
                "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
   if (split >= nsplit) return;  // padding split of a shorter sequence
 
   const int Hkv = cv.n_kv_heads;
@@ -114,10 +114,11 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     for (int u = 0; u < U; ++u) {
       const int p = max(0, min(b + u * SLOTS + slot, kend - 1));
       const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, p) + d0;
+      const T* vr = (PAGED ? v_row<true, T>(cv, layer, seq, hk, p) : cvv + off - d0) + d0;
 #pragma unroll
       for (int nv = 0; nv < NV; ++nv) {
         kk[u][nv] = ld16(ck + off + nv * VEC);
-        vv[u][nv] = ld16(cvv + off + nv * VEC);
+        vv[u][nv] = ld16(vr + nv * VEC);
       }
     }
   };

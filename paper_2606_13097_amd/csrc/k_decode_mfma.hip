@@ -85,7 +85,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
                "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
                "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
   if (split >= nsplit) return;  // padding split of a shorter sequence
 
   const int Hkv = cv.n_kv_heads;
@@ -132,7 +132,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int pv = max(0, min(kb + 4 * kg + r, kend - 1));
-      vv[r] = ld16(cvv + kv_offset<PAGED>(cv, layer, seq, hk, pv) + dg * 8);
+      vv[r] = ld16(v_row<PAGED, bf16_t>(cv, layer, seq, hk, pv) + dg * 8);
     }
   };
   uint4 kA[KS], vA[4], kB[KS], vB[4], kC[KS], vC[4];

@@ -77,10 +77,17 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
     khi[p] = ld16_nt(sk + (int64_t)j * D + HALF + kc * VEC);
   }
   const int vc = t % VT, vr = t / VT;
+  // values: not read or written on pages the segment covers entirely when
+  // the cache maps those onto the library; a run made only of such pages
+  // skips them altogether (a block-uniform branch)
+  const bool alias = PAGED && cv.v_alias;
+  const bool run_aliased = alias && (ch.dst & ~15) >= ch.seg_lo && ((ch.dst + ch.n - 1) & ~15) + 16 <= ch.seg_hi;
+  if (!run_aliased) {
 #pragma unroll
-  for (int p = 0; p < VP; ++p) {
-    const int j = min(p * VR + vr, ch.n - 1);
-    vv[p] = ld16_nt(sv + (int64_t)j * D + vc * VEC);
+    for (int p = 0; p < VP; ++p) {
+      const int j = min(p * VR + vr, ch.n - 1);
+      vv[p] = ld16_nt(sv + (int64_t)j * D + vc * VEC);
+    }
   }
   __syncthreads();  // cos/sin ready
 
@@ -107,17 +114,50 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
       st16(ck + off + HALF + kc * VEC, Store<T>::pack(y2));
     }
   }
+  if (run_aliased) return;
 #pragma unroll
   for (int p = 0; p < VP; ++p) {
     const int j = p * VR + vr;
-    if (j < ch.n) {
+    const int pg0 = (ch.dst + j) & ~15;
+    if (j < ch.n && !(alias && pg0 >= ch.seg_lo && pg0 + 16 <= ch.seg_hi)) {
       const int64_t off = kv_offset<PAGED>(cv, l, ch.seq, h, ch.dst + j);
       st16(cvv + off + vc * VEC, vv[p]);
     }
   }
 }
 
+// Copy the first rows of value pages from the library into the cache's own
+// pages (pages that were mapped onto the library and that a truncation split,
+// so that new tokens can follow the kept rows).  Grid (item, kv head, layer).
+template <typename T, int D>
+__global__ void __launch_bounds__(256) unalias_kernel(const UnaliasItem* __restrict__ items,
+                                                      const T* __restrict__ lib_v, int64_t cap, CacheView cv) {
+  constexpr int VEC = Store<T>::VEC;
+  constexpr int VT = D / VEC;
+  const UnaliasItem it = items[blockIdx.x];
+  const int h = blockIdx.y, l = blockIdx.z;
+  const int Hkv = cv.n_kv_heads;
+  for (int idx = threadIdx.x; idx < it.rows * VT; idx += 256) {
+    const int r = idx / VT, c = idx % VT;
+    const T* src = lib_v + (((int64_t)l * Hkv + h) * cap + it.lib_tok + r) * D + c * VEC;
+    T* dst = reinterpret_cast<T*>(cv.v) + (int64_t)l * cv.layer_stride + (((int64_t)it.page * Hkv + h) * 16 + r) * D +
+             c * VEC;
+    st16(dst, ld16(src));
+  }
+}
+
 static int check(hipError_t e) { return e == hipSuccess ? 0 : (int)e; }
+
+int launch_unalias(int dtype, const UnaliasItem* items, int n_items, const void* lib_v, int64_t cap,
+                   const CacheView& cv, int L, hipStream_t s) {
+  if (n_items == 0) return 0;
+  dim3 grid(n_items, cv.n_kv_heads, L);
+#define UA(T, DD) hipLaunchKernelGGL((unalias_kernel<T, DD>), grid, dim3(256), 0, s, items, (const T*)lib_v, cap, cv)
+  if (dtype == 0) { if (cv.head_dim == 64) UA(float, 64); else UA(float, 128); }
+  else { if (cv.head_dim == 64) UA(bf16_t, 64); else UA(bf16_t, 128); }
+#undef UA
+  return check(hipGetLastError());
+}
 
 int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len, int Hkv,
                       int D, int64_t cap, int64_t tok_off, hipStream_t s) {

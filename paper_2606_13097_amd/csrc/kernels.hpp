@@ -22,7 +22,7 @@ struct GraftChunk {
   int32_t seq;      // target sequence
   int32_t delta;    // rotary turn of the keys (dst - src_pos0 of the segment)
   int32_t n;        // tokens in this run
-  int32_t pad0, pad1;
+  int32_t seg_lo, seg_hi;  // the whole segment's positions [seg_lo, seg_hi)
 };
 constexpr int kGraftChunk = 64;
 
@@ -31,7 +31,13 @@ struct CacheView {
   void* k;               // layer-0 base of K
   void* v;               // layer-0 base of V
   int64_t layer_stride;  // elements from one layer's region to the next
-  const int32_t* page_table;  // device [n_seqs][n_lp] (paged only)
+  // paged only: per sequence a row of 2 n_lp entries, the physical page of
+  // each logical page, then (value aliasing) the library token of its first
+  // position or -1
+  const int32_t* page_table;
+  const int32_t* v_alias;  // page_table + n_lp when values may be aliased, else null
+  const void* lib_v;       // the aliased library's V slabs [L][Hkv][lib_cap][D]
+  int64_t lib_cap;
   int32_t n_seqs, max_tokens, page_size, n_lp;
   int32_t n_kv_heads, head_dim;
 };
@@ -42,7 +48,7 @@ __host__ __device__ inline int64_t cache_offset(const CacheView& c, int layer, i
   int64_t base = (int64_t)layer * c.layer_stride;
   if (c.page_size == 0)
     return base + (((int64_t)seq * c.n_kv_heads + head) * c.max_tokens + pos) * c.head_dim;
-  int32_t page = c.page_table[(int64_t)seq * c.n_lp + pos / c.page_size];
+  int32_t page = c.page_table[(int64_t)seq * 2 * c.n_lp + pos / c.page_size];
   return base + (((int64_t)page * c.n_kv_heads + head) * c.page_size + (pos % c.page_size)) * c.head_dim;
 }
 
@@ -50,10 +56,23 @@ __host__ __device__ inline int64_t cache_offset(const CacheView& c, int layer, i
 template <bool PAGED>
 __device__ __forceinline__ int64_t kv_offset(const CacheView& c, int layer, int seq, int head, int pos) {
   if (PAGED) {
-    const int32_t page = c.page_table[(int64_t)seq * c.n_lp + (pos >> 4)];
+    const int32_t page = c.page_table[(int64_t)seq * 2 * c.n_lp + (pos >> 4)];
     return (int64_t)layer * c.layer_stride + (((int64_t)page * c.n_kv_heads + head) * 16 + (pos & 15)) * c.head_dim;
   }
   return (int64_t)layer * c.layer_stride + (((int64_t)seq * c.n_kv_heads + head) * c.max_tokens + pos) * c.head_dim;
+}
+
+// Value row (layer, seq, head, pos) to read: the cache's own row, or the
+// library's row for a page whose values are mapped onto the library.
+template <bool PAGED, typename T>
+__device__ __forceinline__ const T* v_row(const CacheView& c, int layer, int seq, int head, int pos) {
+  if (PAGED && c.v_alias) {
+    const int32_t a = c.v_alias[(int64_t)seq * 2 * c.n_lp + (pos >> 4)];
+    if (a >= 0)
+      return reinterpret_cast<const T*>(c.lib_v) +
+             (((int64_t)layer * c.n_kv_heads + head) * c.lib_cap + a + (pos & 15)) * c.head_dim;
+  }
+  return reinterpret_cast<const T*>(c.v) + kv_offset<PAGED>(c, layer, seq, head, pos);
 }
 
 // Per fresh (or decode) token, in attention order: tokens grouped by sequence,
@@ -104,6 +123,15 @@ int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void
 
 int launch_graft(int dtype, const GraftChunk* chunks, int n_chunks, const void* lib_k, const void* lib_v,
                  int64_t cap, const CacheView& cv, const double* inv_freq, int L, hipStream_t s, KTime tm = {});
+
+// A value page mapped onto the library that a truncation split: its first
+// `rows` rows are copied from library token lib_tok .. into physical page `page`.
+struct UnaliasItem {
+  int64_t lib_tok;
+  int32_t page, rows;
+};
+int launch_unalias(int dtype, const UnaliasItem* items, int n_items, const void* lib_v, int64_t cap,
+                   const CacheView& cv, int L, hipStream_t s);
 
 // Encode q and k of n tokens at their positions, store k and v in the cache
 // (layer), write encoded q to qws [Hkv][n * g][D].

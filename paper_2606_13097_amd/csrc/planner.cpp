@@ -14,13 +14,16 @@ static std::string fmt(const char* f, long long a = 0, long long b = 0, long lon
   return buf;
 }
 
-Planner::Planner(int32_t n_layers, int32_t n_seqs, int32_t max_tokens, int32_t page_size, int32_t n_pages)
+Planner::Planner(int32_t n_layers, int32_t n_seqs, int32_t max_tokens, int32_t page_size, int32_t n_pages,
+                 bool alias_v)
     : L_(n_layers), S_(n_seqs), T_(max_tokens), P_(page_size), NP_(page_size ? n_pages : 0),
-      NLP_(page_size ? (max_tokens + page_size - 1) / page_size : 0), W_((max_tokens + 63) / 64) {
+      NLP_(page_size ? (max_tokens + page_size - 1) / page_size : 0), W_((max_tokens + 63) / 64),
+      AV_(alias_v && page_size != 0) {
   bits_.assign((size_t)S_ * L_ * W_, 0);
   len_.assign((size_t)S_ * L_, 0);
   cnt_.assign((size_t)S_ * L_, 0);
   page_table_.assign((size_t)S_ * NLP_, -1);
+  valias_.assign((size_t)S_ * NLP_, -1);
   for (int32_t p = 0; p < NP_; ++p) free_.insert(free_.end(), p);
 }
 
@@ -184,7 +187,14 @@ void Planner::mark_all_layers(int32_t seq, int32_t dst, int32_t len) {
     for (int32_t p = dst; p < dst + len; ++p) mark(seq, l, p);
 }
 
+void Planner::alias_pages(int32_t seq, int32_t dst, int32_t len, int64_t lib_tok0) {
+  if (!AV_) return;
+  for (int32_t lp = (dst + P_ - 1) / P_; (lp + 1) * P_ <= dst + len; ++lp)
+    valias_[(size_t)seq * NLP_ + lp] = (int32_t)(lib_tok0 + (int64_t)lp * P_ - dst);
+}
+
 void Planner::reset(int32_t seq) {
+  std::fill(valias_.begin() + (size_t)seq * NLP_, valias_.begin() + (size_t)(seq + 1) * NLP_, -1);
   for (int32_t l = 0; l < L_; ++l) {
     std::fill(bits(seq, l), bits(seq, l) + W_, 0ull);
     len_[idx(seq, l)] = 0;
@@ -196,7 +206,14 @@ void Planner::reset(int32_t seq) {
   }
 }
 
-void Planner::truncate(int32_t seq, int32_t pos) {
+void Planner::truncate(int32_t seq, int32_t pos, std::vector<Unalias>* unalias) {
+  if (P_ && pos % P_ && pos < T_) {
+    int32_t& a = valias_[(size_t)seq * NLP_ + pos / P_];
+    if (a >= 0) {
+      if (unalias) unalias->push_back(Unalias{seq, page_table_[(size_t)seq * NLP_ + pos / P_], pos % P_, a});
+      a = -1;
+    }
+  }
   for (int32_t l = 0; l < L_; ++l) {
     uint64_t* b = bits(seq, l);
     for (int32_t wi = 0; wi < W_; ++wi) {
@@ -217,6 +234,7 @@ void Planner::truncate(int32_t seq, int32_t pos) {
     for (int32_t lp = (pos + P_ - 1) / P_; lp < NLP_; ++lp) {
       int32_t& e = page_table_[(size_t)seq * NLP_ + lp];
       if (e >= 0) { free_.insert(e); e = -1; }
+      valias_[(size_t)seq * NLP_ + lp] = -1;
     }
 }
 

@@ -22,9 +22,20 @@ struct Span {
   int32_t seq, seg, dst, len, delta;
 };
 
+// A page whose values were mapped onto the library and that a truncation
+// splits: its first `rows` rows must be copied from library token lib_tok ..
+// into the cache page before new tokens follow them.
+struct Unalias {
+  int32_t seq, page, rows;
+  int64_t lib_tok;
+};
+
 class Planner {
  public:
-  Planner(int32_t n_layers, int32_t n_seqs, int32_t max_tokens, int32_t page_size, int32_t n_pages);
+  // alias_v: pages that one grafted segment covers entirely read their values
+  // from the library (paged caches only)
+  Planner(int32_t n_layers, int32_t n_seqs, int32_t max_tokens, int32_t page_size, int32_t n_pages,
+          bool alias_v = false);
 
   int32_t n_layers() const { return L_; }
   int32_t n_seqs() const { return S_; }
@@ -32,6 +43,7 @@ class Planner {
   int32_t page_size() const { return P_; }
   int32_t n_pages() const { return NP_; }
   int32_t n_logical_pages() const { return NLP_; }
+  bool alias_v() const { return AV_; }
 
   // Validation.  On success the returned status is FCG_OK and *new_pages holds
   // the (seq, logical page) pairs the call maps, in mapping order; on failure
@@ -46,9 +58,15 @@ class Planner {
   // Commits (after a successful check).
   void map_pages(const std::vector<std::pair<int32_t, int32_t>>& new_pages);
   void mark_all_layers(int32_t seq, int32_t dst, int32_t len);
+  // graft of len tokens at dst whose first token is library token lib_tok0:
+  // with alias_v, the logical pages inside [dst, dst + len) map their values
+  // onto the library
+  void alias_pages(int32_t seq, int32_t dst, int32_t len, int64_t lib_tok0);
   void mark(int32_t seq, int32_t layer, int32_t pos);
   void reset(int32_t seq);
-  void truncate(int32_t seq, int32_t pos);  // keep [0, pos) in every layer; caller checked the range
+  // keep [0, pos) in every layer (the caller checked the range); a split
+  // page mapped onto the library is appended to *unalias and unmapped
+  void truncate(int32_t seq, int32_t pos, std::vector<Unalias>* unalias = nullptr);
 
   // Queries.
   bool written(int32_t seq, int32_t layer, int32_t pos) const;
@@ -56,6 +74,8 @@ class Planner {
   int32_t count(int32_t seq, int32_t layer) const { return cnt_[idx(seq, layer)]; }
   const int32_t* page_row(int32_t seq) const { return page_table_.data() + (size_t)seq * NLP_; }
   int32_t page_of(int32_t seq, int32_t pos) const { return page_table_[(size_t)seq * NLP_ + pos / P_]; }
+  // [NLP] library token of each logical page's first position, -1 = the page's own values
+  const int32_t* alias_row(int32_t seq) const { return valias_.data() + (size_t)seq * NLP_; }
 
  private:
   size_t idx(int32_t seq, int32_t layer) const { return (size_t)seq * L_ + layer; }
@@ -67,9 +87,11 @@ class Planner {
                            std::vector<std::pair<int32_t, int32_t>>* new_pages, std::string* msg) const;
 
   int32_t L_, S_, T_, P_, NP_, NLP_, W_;
+  bool AV_;
   std::vector<uint64_t> bits_;       // [S][L][W] written bits
   std::vector<int32_t> len_, cnt_;   // [S][L]
   std::vector<int32_t> page_table_;  // [S][NLP], -1 = unmapped
+  std::vector<int32_t> valias_;      // [S][NLP], library token or -1
   std::set<int32_t> free_;           // free physical pages, ascending
 };
 

@@ -25,6 +25,7 @@ LIB_PATH = os.path.join(_HERE, "libfcg.so")
 
 FCG_F32, FCG_BF16 = 0, 1
 FCG_LAYOUT_ONLY = 1
+FCG_ALIAS_V = 2
 STATUS = ["FCG_OK", "FCG_EINVAL", "FCG_ERANGE", "FCG_EOVERLAP", "FCG_EHOLE", "FCG_ENOMEM", "FCG_ESTATE",
           "FCG_EHIP"]
 FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE, FCG_EHIP = range(8)
@@ -32,7 +33,8 @@ FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE,
 # every symbol include/fcg.h declares
 EXPORTS = [
     "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
-    "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_device_ptrs",
+    "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_export_v_alias",
+    "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
     "fcg_cache_timing", "fcg_cache_timing_read",
 ]
@@ -70,7 +72,8 @@ def _load():
         "fcg_lib_destroy": [P],
         "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
         "fcg_cache_reset": [P, I32],
-        "fcg_cache_truncate": [P, I32, I32],
+        "fcg_cache_truncate": [P, I32, I32, P],
+        "fcg_cache_export_v_alias": [P, I32, P],
         "fcg_cache_export_layout": [P, I32, I32, P, PI32, P],
         "fcg_cache_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
         "fcg_cache_destroy": [P],
@@ -214,9 +217,16 @@ def fcg_cache_reset(cache: Cache, seq: int) -> None:
     _check(_L.fcg_cache_reset(cache.h, int(seq)))
 
 
-def fcg_cache_truncate(cache: Cache, seq: int, pos: int) -> None:
+def fcg_cache_truncate(cache: Cache, seq: int, pos: int, stream=None) -> None:
     """Keep positions [0, pos) of ``seq`` in every layer (cache-patching reuses that prefix)."""
-    _check(_L.fcg_cache_truncate(cache.h, int(seq), int(pos)))
+    _check(_L.fcg_cache_truncate(cache.h, int(seq), int(pos), _stream(stream)))
+
+
+def fcg_cache_export_v_alias(cache: Cache, seq: int) -> np.ndarray:
+    """-> int32 [n_lp]: library token of each logical page's first position, -1 = own values."""
+    out = np.zeros(max(cache.n_lp, 1), dtype=np.int32)
+    _check(_L.fcg_cache_export_v_alias(cache.h, int(seq), out.ctypes.data))
+    return out[:cache.n_lp]
 
 
 def fcg_cache_export_layout(cache: Cache, seq: int, layer: int):

@@ -48,8 +48,9 @@ def to_device(a: np.ndarray, dtype: str) -> torch.Tensor:
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
 
 
-def read_cache(cache: fcg.Cache, w: synth.Workload, layer: int, seq: int, positions) -> tuple:
-    """K, V of (layer, seq) at ``positions`` as storage arrays [n][Hkv][D]."""
+def read_cache(cache: fcg.Cache, w: synth.Workload, layer: int, seq: int, positions, lib=None) -> tuple:
+    """K, V of (layer, seq) at ``positions`` as storage arrays [n][Hkv][D]; with ``lib``, the
+    values of pages the cache maps onto that library are read from the library."""
     sh = w.shape
     H, D, es = sh.n_kv_heads, sh.head_dim, sh.elem_bytes
     npdt = np.float32 if sh.dtype == "f32" else np.uint16
@@ -68,6 +69,15 @@ def read_cache(cache: fcg.Cache, w: synth.Workload, layer: int, seq: int, positi
             pages = pt[positions // P]
             assert (pages >= 0).all()
             res.append(np.ascontiguousarray(pool[pages, :, positions % P]))
+    if cache.page_size and lib is not None:
+        alias = fcg.fcg_cache_export_v_alias(cache, seq)[positions // cache.page_size]
+        hit = alias >= 0
+        if hit.any():
+            cap = lib.capacity
+            _, lv = fcg.fcg_lib_device_ptrs(lib, layer)
+            slab = d2h(lv, H * cap * D * es).view(npdt).reshape(H, cap, D)
+            toks = alias[hit] + positions[hit] % cache.page_size
+            res[1][hit] = slab[:, toks].transpose(1, 0, 2)
     return res[0], res[1]
 
 

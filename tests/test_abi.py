@@ -43,6 +43,23 @@ def test_status_strings_and_errors_without_gpu():
         fcg.Cache(fcg.model_desc(1, 4, 2, 64, 1e4, "bf16"), 1, 16, page_size=8, n_pages=4,
                   flags=fcg.FCG_LAYOUT_ONLY)
     assert e.value.status == fcg.FCG_EINVAL
+    # value aliasing needs a paged cache, and binds a cache to one library
+    desc = fcg.model_desc(1, 4, 2, 64, 1e4, "bf16")
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.Cache(desc, 1, 16, flags=fcg.FCG_LAYOUT_ONLY | fcg.FCG_ALIAS_V)
+    assert e.value.status == fcg.FCG_EINVAL
+    c = fcg.Cache(desc, 2, 64, page_size=16, n_pages=8, flags=fcg.FCG_LAYOUT_ONLY | fcg.FCG_ALIAS_V)
+    libs = [fcg.Library(desc, 64, 2, flags=fcg.FCG_LAYOUT_ONLY) for _ in range(2)]
+    for lib in libs:
+        fcg.fcg_lib_add_segment(lib, 32, 0)
+    fcg.fcg_graft(c, libs[0], [0], [0], [16])
+    assert fcg.fcg_cache_export_v_alias(c, 0).tolist() == [-1, 0, 16, -1]
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.fcg_graft(c, libs[1], [1], [0], [0])
+    assert e.value.status == fcg.FCG_EINVAL and "one library" in fcg.fcg_last_error()
+    with pytest.raises(fcg.FcgError) as e:
+        fcg.fcg_cache_export_v_alias(c, 2)
+    assert e.value.status == fcg.FCG_ERANGE
 
 
 def test_timing_api_without_device_work():

@@ -4,6 +4,8 @@ Bars: layout and placement bit-exact; grafted and copied values bit-exact; graft
 within 1e-5 normwise (fp32) or one bf16 ulp; attention outputs within 1e-5 normwise per
 head (fp32) or max-abs 2e-2 plus relative Frobenius 1e-2 (bf16).
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -24,8 +26,9 @@ def _gpu():
     yield
 
 
-def _oracle_layout(w, n_decode, layers):
-    ora = Layout(w.shape.n_layers, w.n_seqs, w.max_tokens, w.page_size, w.n_pages, w.lib_lengths, w.lib_src_pos0)
+def _oracle_layout(w, n_decode, layers, alias=False):
+    ora = Layout(w.shape.n_layers, w.n_seqs, w.max_tokens, w.page_size, w.n_pages, w.lib_lengths, w.lib_src_pos0,
+                 alias_v=alias)
     ora.graft(w.graft_seq, w.graft_seg, w.graft_dst)
     for layer in layers:
         ora.append(layer, w.fresh_seq, w.fresh_pos)
@@ -43,14 +46,15 @@ def _compare_layout(cache, ora, w, layers):
             assert n == ora.seq_len(s, layer)
             if w.page_size:
                 np.testing.assert_array_equal(pt, ora.page_table[s])
+                np.testing.assert_array_equal(fcg.fcg_cache_export_v_alias(cache, s), ora.v_alias[s])
 
 
-def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False):
-    from paper_2606_13097_amd import runner
+def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False, alias=False):
+    from paper_2606_13097_amd import fcg, runner
     sh = w.shape
     say(f"[gpu] pipeline {w.name} L={sh.n_layers} seqs={w.n_seqs} decode={n_decode} q_mult={q_mult} "
-        f"shuffle={shuffle} page={w.page_size}")
-    setup = runner.GpuSetup(w)
+        f"shuffle={shuffle} page={w.page_size} alias={alias}")
+    setup = runner.GpuSetup(w, cache_flags=fcg.FCG_ALIAS_V if alias else 0)
     try:
         setup.graft()
         torch.cuda.synchronize()
@@ -63,7 +67,7 @@ def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False):
                 w_items[(s, layer)] = items
                 K, V, wr = ograft.compose(w.max_tokens, sh.n_kv_heads, sh.head_dim, items, w_inv, sh.dtype)
                 pos = np.flatnonzero(wr)
-                gk, gv = read_cache(setup.cache, w, layer, s, pos)
+                gk, gv = read_cache(setup.cache, w, layer, s, pos, setup.lib)
                 np.testing.assert_array_equal(numerics.decode(gv, sh.dtype), V[pos])
                 check_keys(gk, K[pos], sh.dtype, f"graft keys seq {s} layer {layer}")
                 # segments whose delta is 0 are copied bit for bit
@@ -100,7 +104,7 @@ def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False):
             outs[("decode", layer)] = douts
         torch.cuda.synchronize()
         say("[gpu]   decode done")
-        ora = _oracle_layout(w, n_decode, layers)
+        ora = _oracle_layout(w, n_decode, layers, alias)
         _compare_layout(setup.cache, ora, w, layers)
         for layer in layers:
             for s in check_seqs:
@@ -113,7 +117,7 @@ def run_pipeline(w, layers, n_decode, check_seqs, q_mult=1.0, shuffle=False):
                     check_attn(got, ref["decode"][t], sh.dtype, f"decode seq {s} layer {layer} step {t}")
                 # final cache: fresh and decode keys/values placed at their positions
                 pos = np.flatnonzero(ref["written"])
-                gk, gv = read_cache(setup.cache, w, layer, s, pos)
+                gk, gv = read_cache(setup.cache, w, layer, s, pos, setup.lib)
                 np.testing.assert_array_equal(numerics.decode(gv, sh.dtype), ref["V"][pos])
                 check_keys(gk, ref["K"][pos], sh.dtype, f"final keys seq {s} layer {layer}")
         say("[gpu]   parity ok")
@@ -164,6 +168,21 @@ def test_batched_paged_bf16():
     from paper_2606_13097_amd import synth
     w = synth.workload("batched", seed=1, n_layers=1, n_lib=48)
     run_pipeline(w, [0], 3, [0, 7, 31])
+
+
+def test_batched_paged_bf16_values_read_from_the_library():
+    """The batched paged workload with value pages mapped onto the library
+    (FCG_ALIAS_V): page tables and aliases bit-exact, values bit-exact where
+    they are read (library or cache page), outputs within the bf16 bars."""
+    from paper_2606_13097_amd import synth
+    w = synth.workload("batched", seed=2, n_layers=1, n_lib=48)
+    run_pipeline(w, [0], 3, [0, 5, 31], alias=True)
+
+
+def test_tiny_fp32_paged_values_read_from_the_library():
+    from paper_2606_13097_amd import synth
+    w = dataclasses.replace(synth.workload("tiny", seed=3), page_size=16)
+    run_pipeline(w, [0], 4, list(range(w.n_seqs)), alias=True)
 
 
 def test_34b_shape_outliers_bf16():
@@ -356,8 +375,9 @@ def _tokens(w, tag, layer, item, rows):
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("dtype,page", [("bf16", 0), ("bf16", 16), ("f32", 16)])
-def test_cache_patching_cut_regenerate_decode(dtype, page):
+@pytest.mark.parametrize("dtype,page,alias", [("bf16", 0, False), ("bf16", 16, False), ("f32", 16, False),
+                                               ("bf16", 16, True), ("f32", 16, True)])
+def test_cache_patching_cut_regenerate_decode(dtype, page, alias):
     """Cache-patching (Sec. 4.2, Eq. 6): after graft -> prefill -> two decode steps,
     each sequence is cut back to an error position -- inside its grafted context on
     a page boundary, inside its fresh span, at its full length (nothing cut), at 0
@@ -368,12 +388,15 @@ def test_cache_patching_cut_regenerate_decode(dtype, page):
     shape = synth.Shape(2, 32, 8, 128, 1e6, "bf16") if dtype == "bf16" else synth.Shape(2, 4, 2, 64, 1e4, "f32")
     w = synth.custom(shape, 17, [90, 130, 200, 64], [[0, 1], [2], [3, 1], [2, 0]], n_fresh=5, n_decode=2,
                      page_size=page)
-    keep = [96, 203, 201, 0]               # contexts 220, 200, 194, 290; 5 fresh tokens, 2 decoded
+    # contexts 220, 200, 194, 290; 5 fresh tokens, 2 decoded.  With value
+    # aliasing, the cut at 100 splits a page whose values are read from the
+    # library: its kept rows are copied into the page before new tokens follow
+    keep = [100 if alias else 96, 203, 201, 0]
     n_new = [37, 9, 1, 70]
     layers = [0, 1]
     sh = w.shape
-    say(f"[gpu] cache patching {dtype} page={page} keep={keep} new={n_new}")
-    setup = runner.GpuSetup(w)
+    say(f"[gpu] cache patching {dtype} page={page} alias={alias} keep={keep} new={n_new}")
+    setup = runner.GpuSetup(w, cache_flags=fcg.FCG_ALIAS_V if alias else 0)
     try:
         setup.graft()
         for layer in layers:
@@ -405,7 +428,7 @@ def test_cache_patching_cut_regenerate_decode(dtype, page):
                 outs[("decode", layer, t)] = out
         torch.cuda.synchronize()
         say("[gpu]   patch done")
-        ora = _oracle_layout(w, 2, layers)
+        ora = _oracle_layout(w, 2, layers, alias)
         for s, e in enumerate(keep):
             ora.truncate(s, e)
         for layer in layers:
@@ -429,7 +452,7 @@ def test_cache_patching_cut_regenerate_decode(dtype, page):
                     check_attn(storage_np(outs[("decode", layer, t)][s]), ref["decode"][t], dtype,
                                f"patch decode seq {s} layer {layer} step {t}")
                 wpos = np.flatnonzero(ref["written"])
-                gk, gv = read_cache(setup.cache, w, layer, s, wpos)
+                gk, gv = read_cache(setup.cache, w, layer, s, wpos, setup.lib)
                 np.testing.assert_array_equal(numerics.decode(gv, dtype), ref["V"][wpos])
                 check_keys(gk, ref["K"][wpos], dtype, f"patched keys seq {s} layer {layer}")
         say("[gpu]   patch parity ok")

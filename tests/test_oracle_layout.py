@@ -219,3 +219,54 @@ def test_truncate_against_enumeration(data):
     if page:
         pages = L.page_table[L.page_table >= 0].tolist()
         assert len(set(pages)) == len(pages)                       # injective
+
+
+def test_value_aliases_by_hand():
+    # segments of 40 and 20 tokens stored back to back in the library (tokens 0.., 40..)
+    L = Layout(2, 2, 96, 16, 32, [40, 20], [0, 0], alias_v=True)
+    L.graft([0, 0, 1], [0, 1, 0], [8, 48, 16])
+    # seq 0: segment 0 at 8..47 covers logical page 1 (16..31) and 2 (32..47) entirely;
+    # segment 1 at 48..67 covers page 3 (48..63) and part of page 4
+    assert L.v_alias[0].tolist() == [-1, 8, 24, 40, -1, -1]
+    # seq 1: segment 0 at 16..55 covers pages 1 and 2; page 3 (48..63) only in part
+    assert L.v_alias[1].tolist() == [-1, 0, 16, -1, -1, -1]
+    # a cut inside an aliased page takes the page back: it will hold new tokens
+    L.truncate(0, 36)
+    assert L.v_alias[0].tolist() == [-1, 8, -1, -1, -1, -1]
+    # a cut on a page boundary keeps the pages before it as they were
+    L.truncate(1, 32)
+    assert L.v_alias[1].tolist() == [-1, 0, -1, -1, -1, -1]
+    L.reset(1)
+    assert (L.v_alias[1] == -1).all()
+    # without the flag nothing is aliased
+    M = Layout(2, 1, 96, 16, 32, [40, 20], [0, 0])
+    M.graft([0], [0], [8])
+    assert (M.v_alias == -1).all()
+
+
+@settings(max_examples=60, deadline=None)
+@given(st.data())
+def test_value_aliases_against_enumeration(data):
+    """A logical page aliases the library exactly when one grafted segment
+    covers all 16 of its positions and no cut has split or dropped it; the
+    alias then names the library token at the page's first position."""
+    seg_len = data.draw(st.lists(st.integers(1, 40), min_size=1, max_size=4))
+    tok0 = np.concatenate([[0], np.cumsum(seg_len)])
+    L = Layout(1, 1, 128, 16, 64, seg_len, [0] * len(seg_len), alias_v=True)
+    want = {}
+    for _ in range(data.draw(st.integers(1, 6))):
+        if data.draw(st.booleans()):
+            g = data.draw(st.integers(0, len(seg_len) - 1))
+            d = data.draw(st.integers(0, 128 - seg_len[g]))
+            try:
+                L.graft([0], [g], [d])
+            except FcgError:
+                continue
+            for lp in range(8):
+                if lp * 16 >= d and lp * 16 + 16 <= d + seg_len[g]:
+                    want[lp] = int(tok0[g]) + lp * 16 - d
+        else:
+            cut = data.draw(st.integers(0, 128))
+            L.truncate(0, cut)
+            want = {lp: a for lp, a in want.items() if lp * 16 + 16 <= cut}
+        assert L.v_alias[0].tolist() == [want.get(lp, -1) for lp in range(8)]

@@ -7,10 +7,12 @@ from oracle.layout import FcgError as OracleError, Layout
 from paper_2606_13097_amd import fcg, synth
 
 
-def _pair(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src):
+def _pair(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src, alias=False):
     desc = fcg.model_desc(n_layers, 4, 2, 64, 1e4, "f32")
-    cache = fcg.Cache(desc, n_seqs, max_tokens, page, n_pages, flags=fcg.FCG_LAYOUT_ONLY)
-    ora = Layout(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src)
+    alias = alias and page > 0
+    flags = fcg.FCG_LAYOUT_ONLY | (fcg.FCG_ALIAS_V if alias else 0)
+    cache = fcg.Cache(desc, n_seqs, max_tokens, page, n_pages, flags=flags)
+    ora = Layout(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src, alias_v=alias)
     return desc, cache, ora
 
 
@@ -29,6 +31,7 @@ def _compare(cache, ora, n_seqs, n_layers):
             assert n == ora.seq_len(s, l)
             if cache.page_size:
                 np.testing.assert_array_equal(pt, ora.page_table[s])
+                np.testing.assert_array_equal(fcg.fcg_cache_export_v_alias(cache, s), ora.v_alias[s])
 
 
 def _run_both(fn_c, fn_o):
@@ -108,7 +111,7 @@ def test_graft_plans_match_oracle(data):
     page = data.draw(st.sampled_from([0, 16]))
     max_tokens = data.draw(st.integers(8, 160))
     n_pages = data.draw(st.integers(1, 16))
-    desc, cache, ora = _pair(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src)
+    desc, cache, ora = _pair(n_layers, n_seqs, max_tokens, page, n_pages, seg_len, src, alias=data.draw(st.booleans()))
     lib = _lib(desc, seg_len, src)
     for _ in range(data.draw(st.integers(1, 6))):
         n = data.draw(st.integers(0, 4))
