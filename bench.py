@@ -93,6 +93,32 @@ def graft_bytes(tw, kvb, n_layers, alias_v):
     return total * n_layers
 
 
+def locality_update(w, task_ws, reps=200):
+    """Host cost of the cache-management update (locality scores and residency over
+    the library's segments) after a task, with the window filled by the tasks' traces."""
+    import numpy as np
+    from paper_2606_13097_amd import fcg
+    n = len(w.lib_lengths)
+    loc = fcg.Locality(n, 20)
+    rng = np.random.default_rng(0)
+    for f in range(n):
+        fcg.fcg_locality_set_ppl(loc, f, float(rng.uniform(2.0, 30.0)))
+    cost = (w.lib_lengths.astype(np.int64) * w.shape.token_bytes)
+    budget = int(cost.sum() // 2)
+    traces = [tw.graft_seg[tw.graft_seq == 0].astype(np.int32) for tw in task_ws]
+    for i in range(20):
+        fcg.fcg_locality_record(loc, traces[i % len(traces)])
+    t0 = time.perf_counter()
+    for i in range(reps):
+        fcg.fcg_locality_record(loc, traces[i % len(traces)])
+        fcg.fcg_locality_scores(loc)
+        keep = fcg.fcg_locality_residency(loc, budget, cost)
+    dt = (time.perf_counter() - t0) / reps
+    loc.close()
+    return {"update_us": round(dt * 1e6, 2), "functions": n, "window": 20, "budget_fraction": 0.5,
+            "resident_after": int(keep.sum())}
+
+
 def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
     """The oracle, as it stands, on a bounded sample of the same workload."""
     import numpy as np
@@ -417,6 +443,7 @@ def main():
                             "traffic": measured_traffic("decode_7b_traffic.json"),
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},
     }
+    res["locality"] = locality_update(w, task_ws)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(w, task_ws)

@@ -73,6 +73,7 @@ typedef struct {
 
 typedef struct fcg_lib fcg_lib;
 typedef struct fcg_cache fcg_cache;
+typedef struct fcg_locality fcg_locality;
 
 /* ---------------------------------------------------------------- library */
 
@@ -205,6 +206,40 @@ fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int
                       int32_t* positions_out, void* stream);
 
 /* ------------------------------------------------------------- diagnostics */
+
+/* ------------------------------------------------- code-cache management */
+
+/* Locality score of the cache entries (Sec. 4.1, Eq. 3; App. B.1, Eq. 8-10;
+ * the update step of Alg. 1), host only:
+ *   l(f) = (1 - l_curr(f)) (alpha l_freq(f) + beta sum_j l_asso(j | f)
+ *          + gamma l_sema(f)) + l_curr(f),
+ *   l_freq(f) = count(f) / max_j count(j),
+ *   l_asso(j | f) = cooccur(f, j) / count(f),
+ *   l_sema(f) = PPL(f) / max_j PPL(j).
+ * Functions are ids 0 .. n_funcs - 1 (a caller's map to library segments).
+ * Statistics cover the last `window` recorded execution traces (one per task;
+ * the paper uses 20); cooccur(f, j) counts calls of j that immediately follow
+ * a call of f in one trace; l_curr(f) = 1 iff f occurs in the latest trace;
+ * a component with a zero denominator is 0.  Weights: >= 0, summing to 1 (the
+ * paper uses 0.4, 0.3, 0.3).
+ * Errors: EINVAL (n_funcs or window < 1, bad weights, null output), ENOMEM. */
+fcg_status fcg_locality_create(int32_t n_funcs, int32_t window, double alpha, double beta, double gamma,
+                               fcg_locality** out);
+/* Record one task's execution trace: func_ids[n] (host) in call order.
+ * Errors: EINVAL (null handle, n < 0, null ids), ERANGE (an id). */
+fcg_status fcg_locality_record(fcg_locality* loc, int32_t n, const int32_t* func_ids);
+/* Perplexity of function func's implementation (>= 0; 0 until set).
+ * Errors: EINVAL (null handle, negative or NaN ppl), ERANGE (func). */
+fcg_status fcg_locality_set_ppl(fcg_locality* loc, int32_t func, double ppl);
+/* scores[n_funcs] (host) receives l(f), each in [0, 1].  Errors: EINVAL. */
+fcg_status fcg_locality_scores(const fcg_locality* loc, double* scores);
+/* Which entries stay in device memory under a budget: in descending score
+ * (ties: ascending id), an entry is kept when its cost[f] (host, >= 0, e.g.
+ * bytes or tokens) still fits in what the kept ones leave of budget.
+ * resident[n_funcs] (host) receives 1 / 0.  Errors: EINVAL (null arguments,
+ * negative budget or cost). */
+fcg_status fcg_locality_residency(const fcg_locality* loc, int64_t budget, const int64_t* cost, uint8_t* resident);
+fcg_status fcg_locality_destroy(fcg_locality* loc);
 
 /* Kernel timing (measurement, not part of the method).  While enabled, every
  * call on this cache records HIP events on its stream around its kernels:

@@ -36,7 +36,7 @@ COMMON = [
 LIBS = {
     os.path.join(PKG, "libfcg.so"): [
         os.path.join(CSRC, f) for f in
-        ("api.cpp", "planner.cpp", "k_graft.hip", "k_append.hip", "k_attn_rows.hip", "k_attn_mfma.hip",
+        ("api.cpp", "planner.cpp", "locality.cpp", "k_graft.hip", "k_append.hip", "k_attn_rows.hip", "k_attn_mfma.hip",
          "k_decode.hip", "k_decode_mfma.hip")
     ],
     os.path.join(PKG, "synth", "libfcg_synth.so"): [os.path.join(PKG, "synth", "synth.hip")],

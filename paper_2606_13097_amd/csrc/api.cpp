@@ -13,6 +13,7 @@
 #include <unordered_map>
 #include <vector>
 
+#include "errors.hpp"
 #include "fcg.h"
 #include "kernels.hpp"
 #include "planner.hpp"
@@ -27,6 +28,12 @@ fcg_status fail(fcg_status s, const std::string& msg) {
   g_err = msg;
   return s;
 }
+
+}  // namespace
+
+fcg_status fcg::report(fcg_status s, const std::string& msg) { return fail(s, msg); }
+
+namespace {
 
 fcg_status hip_fail(hipError_t e, const char* what) {
   return fail(FCG_EHIP, std::string(what) + ": " + hipGetErrorString(e));

@@ -37,6 +37,8 @@ EXPORTS = [
     "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
     "fcg_cache_timing", "fcg_cache_timing_read",
+    "fcg_locality_create", "fcg_locality_record", "fcg_locality_set_ppl", "fcg_locality_scores",
+    "fcg_locality_residency", "fcg_locality_destroy",
 ]
 FCG_TIME_GRAFT, FCG_TIME_PREFILL_ATTN, FCG_TIME_PREFILL, FCG_TIME_DECODE, FCG_TIME_DECODE_ATTN = range(5)
 
@@ -83,6 +85,12 @@ def _load():
         "fcg_decode": [P, I32, I32, P, P, P, P, P, P, P],
         "fcg_cache_timing": [P, I32],
         "fcg_cache_timing_read": [P, I32, PI32, C.POINTER(C.c_double)],
+        "fcg_locality_create": [I32, I32, C.c_double, C.c_double, C.c_double, C.POINTER(P)],
+        "fcg_locality_record": [P, I32, P],
+        "fcg_locality_set_ppl": [P, I32, C.c_double],
+        "fcg_locality_scores": [P, P],
+        "fcg_locality_residency": [P, I64, P, P],
+        "fcg_locality_destroy": [P],
     }
     for name, args in sig.items():
         f = getattr(lib, name)
@@ -282,6 +290,50 @@ def fcg_cache_timing_read(cache: Cache, kind: int):
     n, ms = C.c_int32(), C.c_double()
     _check(_L.fcg_cache_timing_read(cache.h, int(kind), C.byref(n), C.byref(ms)))
     return n.value, ms.value
+
+
+class Locality:
+    """Handle of a locality scorer (``fcg_locality``)."""
+
+    h = None
+
+    def __init__(self, n_funcs: int, window: int = 20, alpha: float = 0.4, beta: float = 0.3, gamma: float = 0.3):
+        h = C.c_void_p()
+        _check(_L.fcg_locality_create(int(n_funcs), int(window), float(alpha), float(beta), float(gamma),
+                                      C.byref(h)))
+        self.h, self.n_funcs = h, int(n_funcs)
+        self._lib = _L
+
+    def close(self):
+        if self.h:
+            self._lib.fcg_locality_destroy(self.h)
+            self.h = None
+
+    __del__ = close
+
+
+def fcg_locality_record(loc: Locality, func_ids) -> None:
+    a = np.ascontiguousarray(func_ids, dtype=np.int32)
+    _check(_L.fcg_locality_record(loc.h, len(a), a.ctypes.data if len(a) else None))
+
+
+def fcg_locality_set_ppl(loc: Locality, func: int, ppl: float) -> None:
+    _check(_L.fcg_locality_set_ppl(loc.h, int(func), float(ppl)))
+
+
+def fcg_locality_scores(loc: Locality) -> np.ndarray:
+    out = np.zeros(loc.n_funcs, dtype=np.float64)
+    _check(_L.fcg_locality_scores(loc.h, out.ctypes.data))
+    return out
+
+
+def fcg_locality_residency(loc: Locality, budget: int, cost) -> np.ndarray:
+    c = np.ascontiguousarray(cost, dtype=np.int64)
+    if len(c) != loc.n_funcs:
+        raise ValueError("one cost per function")
+    out = np.zeros(loc.n_funcs, dtype=np.uint8)
+    _check(_L.fcg_locality_residency(loc.h, int(budget), c.ctypes.data, out.ctypes.data))
+    return out
 
 
 def fcg_status_string(status: int) -> str:
