@@ -444,6 +444,28 @@ def main():
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},
     }
     res["locality"] = locality_update(w, task_ws)
+    # host tier: one task's segments to pinned host memory and back
+    segs = sorted(set(int(g) for g in task_ws[0].graft_seg))
+    tokens = sum(int(w.lib_lengths[g]) for g in segs)
+    fcg.fcg_lib_host_reserve(lib, tokens)
+    torch.cuda.synchronize()
+    o0 = ev()
+    for g in segs:
+        fcg.fcg_lib_offload(lib, g, sp)
+    o1 = ev()
+    for g in segs:
+        fcg.fcg_lib_reload(lib, g, sp)
+    o2 = ev()
+    torch.cuda.synchronize()
+    tb = tokens * sh.token_bytes
+    res["offload_reload"] = {
+        "segments": len(segs), "bytes": tb,
+        "offload_ms": round(o0.elapsed_time(o1), 3), "reload_ms": round(o1.elapsed_time(o2), 3),
+        "offload_gbs": round(tb / (o0.elapsed_time(o1) / 1e3) / 1e9, 2),
+        "reload_gbs": round(tb / (o1.elapsed_time(o2) / 1e3) / 1e9, 2),
+        "note": "one task's grafted segments (all layers, K and V) to pinned host slabs and back, "
+                "including the call overhead; the paper's RTX 4090 figures per synthesis are 20.33 ms "
+                "(GPU to host) and 23.42 ms (host to GPU)"}
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(w, task_ws)

@@ -105,9 +105,37 @@ fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, cons
                                const void* v, void* stream, int32_t* seg_id);
 
 /* Where segment seg_id sits: tokens tok_off .. tok_off + len - 1 of every
- * [Hkv][capacity][D] slab; keys encoded from src_pos0.  Any output may be NULL. */
+ * [Hkv][capacity][D] slab (tok_off = -1 while offloaded); keys encoded from
+ * src_pos0.  Any output may be NULL. */
 fcg_status fcg_lib_segment_info(const fcg_lib* lib, int32_t seg_id, int64_t* tok_off,
                                 int32_t* len, int32_t* src_pos0);
+
+/* Host tier of the library (the DRAM side of the code cache: low-scored
+ * entries are offloaded and reloaded when needed; Sec. 4.1, App. C.5).
+ * fcg_lib_host_reserve allocates pinned host slabs of host_tokens tokens
+ * (layout as the device slabs); each segment gets a host copy on its first
+ * offload, kept until the library is destroyed (segments never change).
+ * Errors: EINVAL (host_tokens < 1), ESTATE (reserved already), ENOMEM, EHIP. */
+fcg_status fcg_lib_host_reserve(fcg_lib* lib, int64_t host_tokens);
+
+/* Move segment seg_id out of device memory: copy it to its host slot on
+ * stream (first offload only) and free its device range for later segments
+ * and reloads (first fit; a reused range is written only after the copy has
+ * read it).  fcg_graft of an offloaded segment fails with ESTATE.  Async:
+ * calls on one library are ordered by the caller (one stream, or events).
+ * Errors: ERANGE (seg_id), ESTATE (not in device memory, no host tier, or an
+ * FCG_ALIAS_V cache reads its values in place: reset those sequences first),
+ * ENOMEM (host tier full), EHIP. */
+fcg_status fcg_lib_offload(fcg_lib* lib, int32_t seg_id, void* stream);
+
+/* Bring an offloaded segment back into device memory on stream, at the first
+ * free device range that fits (fcg_lib_segment_info gives the new offset).
+ * Errors: ERANGE, ESTATE (already in device memory), ENOMEM (no range fits), EHIP. */
+fcg_status fcg_lib_reload(fcg_lib* lib, int32_t seg_id, void* stream);
+
+/* *in_device = 1 iff seg_id is in device memory; *on_host = 1 iff it has a host
+ * copy (either may be NULL).  Errors: EINVAL, ERANGE. */
+fcg_status fcg_lib_segment_state(const fcg_lib* lib, int32_t seg_id, int32_t* in_device, int32_t* on_host);
 
 /* Device base pointers of layer's K and V slab ([Hkv][capacity][D]). */
 fcg_status fcg_lib_device_ptrs(const fcg_lib* lib, int32_t layer, void** k, void** v);
@@ -178,7 +206,7 @@ fcg_status fcg_cache_destroy(fcg_cache* cache);
  * meet each other or written positions of any layer), ENOMEM (pages), EINVAL
  * (lib and cache shapes differ, null arrays, a layout-only library with a
  * cache that has device memory, an FCG_ALIAS_V cache bound to another
- * library). */
+ * library), ESTATE (after all of the above pass: a segment is offloaded). */
 fcg_status fcg_graft(fcg_cache* cache, const fcg_lib* lib, int32_t n_items, const int32_t* seq,
                      const int32_t* seg, const int32_t* dst, void* stream);
 

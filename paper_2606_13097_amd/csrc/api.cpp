@@ -7,6 +7,7 @@
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <map>
 #include <new>
 #include <string>
 #include <tuple>
@@ -155,19 +156,61 @@ struct Blob {
 }  // namespace
 
 struct Segment {
-  int64_t tok_off;
+  int64_t tok_off;  // first token in the device slabs, -1 while offloaded
   int32_t len, src_pos0;
+  int64_t host_off = -1;  // first token in the pinned host slabs, -1 without a host copy
+  mutable int32_t pins = 0;  // FCG_ALIAS_V caches reading this segment's values in place
 };
 
 struct fcg_lib {
   fcg_model_desc desc;
-  int64_t cap = 0, used = 0;
+  int64_t cap = 0, used = 0;              // device slab tokens: capacity, high-water mark
+  std::map<int64_t, int64_t> free_tok;    // device token ranges below `used` freed by offloads (start -> length)
   int32_t max_segments = 0;
   uint32_t flags = 0;
   std::vector<Segment> segs;
   void* k = nullptr;
   void* v = nullptr;
   int device = 0;
+  // host tier (fcg_lib_host_reserve): pinned [L][Hkv][host_cap][D] slabs, filled once per segment
+  int64_t host_cap = 0, host_used = 0;
+  void* host_k = nullptr;
+  void* host_v = nullptr;
+  hipEvent_t freed = nullptr;  // after the copies that read the last freed device range
+
+  // first fit among freed ranges, else past the high-water mark; -1 if nothing fits
+  int64_t alloc(int64_t len) {
+    for (auto it = free_tok.begin(); it != free_tok.end(); ++it)
+      if (it->second >= len) {
+        const int64_t off = it->first, rest = it->second - len;
+        free_tok.erase(it);
+        if (rest) free_tok[off + len] = rest;
+        return off;
+      }
+    if (used + len > cap) return -1;
+    used += len;
+    return used - len;
+  }
+  void release(int64_t off, int64_t len) {
+    auto it = free_tok.emplace(off, len).first;
+    auto nx = std::next(it);
+    if (nx != free_tok.end() && it->first + it->second == nx->first) {
+      it->second += nx->second;
+      free_tok.erase(nx);
+    }
+    if (it != free_tok.begin()) {
+      auto pv = std::prev(it);
+      if (pv->first + pv->second == it->first) {
+        pv->second += it->second;
+        free_tok.erase(it);
+        it = pv;
+      }
+    }
+    if (it->first + it->second == used) {  // the top range returns to the high-water mark
+      used = it->first;
+      free_tok.erase(it);
+    }
+  }
 };
 
 struct fcg_cache {
@@ -190,6 +233,7 @@ struct fcg_cache {
   float* dpart = nullptr;     // decode split partials
   size_t dpart_bytes = 0;
   const fcg_lib* alias_lib = nullptr;  // FCG_ALIAS_V: the library value pages map onto (bound by the first graft)
+  std::vector<std::vector<int32_t>> alias_segs;  // per sequence: segments it pins in alias_lib
   int32_t* d_count = nullptr; // decode merge arrival counters [kMaxDecodeSeqs][Hkv] (kCountStride apart), zero between launches
   // kernel timing (fcg_cache_timing): recorded (start, end) event pairs per kind
   bool timing = false;
@@ -385,18 +429,131 @@ fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, cons
   if ((k == nullptr) != (v == nullptr)) return fail(FCG_EINVAL, "k and v must both be given or both be null");
   if (k && (lib->flags & FCG_LAYOUT_ONLY)) return fail(FCG_EINVAL, "a layout-only library takes no data");
   if ((int32_t)lib->segs.size() >= lib->max_segments) return fail(FCG_ENOMEM, "max_segments reached");
-  if (lib->used + len > lib->cap) return fail(FCG_ENOMEM, "library capacity exhausted");
-  const Segment sg{lib->used, len, src_pos0};
-  if (k) {
+  const bool reuse = !lib->free_tok.empty();
+  const int64_t off = lib->alloc(len);
+  if (off < 0) return fail(FCG_ENOMEM, "library capacity exhausted");
+  const Segment sg{off, len, src_pos0};
+  if (!(lib->flags & FCG_LAYOUT_ONLY)) {
     HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+    // a range an offload freed is written only after that offload has read it
+    if (reuse && lib->freed) HIP_TRY(hipStreamWaitEvent((hipStream_t)stream, lib->freed, 0), "hipStreamWaitEvent");
+  }
+  if (k) {
     const fcg_model_desc& d = lib->desc;
     int rc = launch_lib_ingest(d.dtype, k, v, lib->k, lib->v, d.n_layers, len, d.n_kv_heads, d.head_dim, lib->cap,
                                sg.tok_off, (hipStream_t)stream);
-    if (rc) return hip_fail((hipError_t)rc, "ingest launch");
+    if (rc) {
+      lib->release(off, len);
+      return hip_fail((hipError_t)rc, "ingest launch");
+    }
   }
   lib->segs.push_back(sg);
-  lib->used += len;
   if (seg_id) *seg_id = (int32_t)lib->segs.size() - 1;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_host_reserve(fcg_lib* lib, int64_t host_tokens) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (host_tokens < 1) return fail(FCG_EINVAL, "host_tokens must be >= 1");
+  if (lib->host_cap) return fail(FCG_ESTATE, "the host tier is already reserved");
+  if (!(lib->flags & FCG_LAYOUT_ONLY)) {
+    HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+    const fcg_model_desc& d = lib->desc;
+    const size_t bytes = (size_t)d.n_layers * d.n_kv_heads * host_tokens * d.head_dim * esize(d.dtype);
+    if (hipHostMalloc(&lib->host_k, bytes, hipHostMallocDefault) != hipSuccess ||
+        hipHostMalloc(&lib->host_v, bytes, hipHostMallocDefault) != hipSuccess) {
+      if (lib->host_k) hipHostFree(lib->host_k);
+      lib->host_k = nullptr;
+      return fail(FCG_ENOMEM, "pinned host slabs");
+    }
+    if (hipEventCreateWithFlags(&lib->freed, hipEventDisableTiming) != hipSuccess) {
+      hipHostFree(lib->host_k);
+      hipHostFree(lib->host_v);
+      lib->host_k = lib->host_v = nullptr;
+      return fail(FCG_EHIP, "hipEventCreate");
+    }
+  }
+  lib->host_cap = host_tokens;
+  return FCG_OK;
+}
+
+namespace {
+
+// Copy a segment between the device slabs and the host slabs: rows are the
+// (layer, kv head) runs of len tokens, at the two slabs' own pitches.
+fcg_status copy_segment(fcg_lib* lib, const Segment& sg, bool to_host, hipStream_t s) {
+  const fcg_model_desc& d = lib->desc;
+  const size_t es = esize(d.dtype), row = (size_t)d.head_dim * es;
+  const size_t dpitch = (size_t)lib->cap * row, hpitch = (size_t)lib->host_cap * row;
+  const size_t width = (size_t)sg.len * row, height = (size_t)d.n_layers * d.n_kv_heads;
+  for (int kv = 0; kv < 2; ++kv) {
+    char* dev = (char*)(kv ? lib->v : lib->k) + sg.tok_off * row;
+    char* host = (char*)(kv ? lib->host_v : lib->host_k) + sg.host_off * row;
+    const hipError_t e = to_host ? hipMemcpy2DAsync(host, hpitch, dev, dpitch, width, height, hipMemcpyDeviceToHost, s)
+                                 : hipMemcpy2DAsync(dev, dpitch, host, hpitch, width, height, hipMemcpyHostToDevice, s);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpy2DAsync(segment)");
+  }
+  return FCG_OK;
+}
+
+}  // namespace
+
+fcg_status fcg_lib_offload(fcg_lib* lib, int32_t seg_id, void* stream) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (seg_id < 0 || seg_id >= (int32_t)lib->segs.size()) return fail(FCG_ERANGE, "segment id out of range");
+  Segment& sg = lib->segs[seg_id];
+  if (sg.tok_off < 0) return fail(FCG_ESTATE, "segment is not in device memory");
+  if (sg.pins) return fail(FCG_ESTATE, "a cache reads this segment's values in place (FCG_ALIAS_V)");
+  if (!lib->host_cap) return fail(FCG_ESTATE, "no host tier (fcg_lib_host_reserve)");
+  const bool copy = sg.host_off < 0;
+  if (copy && lib->host_used + sg.len > lib->host_cap) return fail(FCG_ENOMEM, "host tier full");
+  hipStream_t s = (hipStream_t)stream;
+  if (copy) {
+    sg.host_off = lib->host_used;
+    if (!(lib->flags & FCG_LAYOUT_ONLY)) {
+      HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+      if (fcg_status st = copy_segment(lib, sg, true, s)) {
+        sg.host_off = -1;
+        return st;
+      }
+    }
+    lib->host_used += sg.len;
+  }
+  if (!(lib->flags & FCG_LAYOUT_ONLY)) HIP_TRY(hipEventRecord(lib->freed, s), "hipEventRecord");
+  lib->release(sg.tok_off, sg.len);
+  sg.tok_off = -1;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_reload(fcg_lib* lib, int32_t seg_id, void* stream) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (seg_id < 0 || seg_id >= (int32_t)lib->segs.size()) return fail(FCG_ERANGE, "segment id out of range");
+  Segment& sg = lib->segs[seg_id];
+  if (sg.tok_off >= 0) return fail(FCG_ESTATE, "segment is already in device memory");
+  const int64_t off = lib->alloc(sg.len);
+  if (off < 0) return fail(FCG_ENOMEM, "library capacity exhausted");
+  sg.tok_off = off;
+  if (!(lib->flags & FCG_LAYOUT_ONLY)) {
+    HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+    hipStream_t s = (hipStream_t)stream;
+    fcg_status st = FCG_OK;
+    if (hipStreamWaitEvent(s, lib->freed, 0) != hipSuccess) st = fail(FCG_EHIP, "hipStreamWaitEvent");
+    if (!st) st = copy_segment(lib, sg, false, s);
+    if (st) {
+      lib->release(off, sg.len);
+      sg.tok_off = -1;
+      return st;
+    }
+  }
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_segment_state(const fcg_lib* lib, int32_t seg_id, int32_t* in_device, int32_t* on_host) {
+  if (!lib) return fail(FCG_EINVAL, "null library");
+  if (seg_id < 0 || seg_id >= (int32_t)lib->segs.size()) return fail(FCG_ERANGE, "segment id out of range");
+  const Segment& sg = lib->segs[seg_id];
+  if (in_device) *in_device = sg.tok_off >= 0;
+  if (on_host) *on_host = sg.host_off >= 0;
   return FCG_OK;
 }
 
@@ -431,6 +588,9 @@ fcg_status fcg_lib_destroy(fcg_lib* lib) {
   hipDeviceSynchronize();
   if (lib->k) hipFree(lib->k);
   if (lib->v) hipFree(lib->v);
+  if (lib->host_k) hipHostFree(lib->host_k);
+  if (lib->host_v) hipHostFree(lib->host_v);
+  if (lib->freed) hipEventDestroy(lib->freed);
   delete lib;
   return FCG_OK;
 }
@@ -483,6 +643,10 @@ fcg_status fcg_cache_reset(fcg_cache* c, int32_t seq) {
   if (!c) return fail(FCG_EINVAL, "null cache");
   if (seq < 0 || seq >= c->n_seqs) return fail(FCG_ERANGE, "sequence out of range");
   c->plan.reset(seq);
+  if (!c->alias_segs.empty()) {
+    for (int32_t g : c->alias_segs[seq]) --c->alias_lib->segs[g].pins;
+    c->alias_segs[seq].clear();
+  }
   // the device page-table row is rewritten on the next mapping of this
   // sequence; stale entries are never read because unwritten positions are
   // never read
@@ -574,6 +738,8 @@ fcg_status fcg_cache_timing_read(fcg_cache* c, int32_t kind, int32_t* count, dou
 
 fcg_status fcg_cache_destroy(fcg_cache* c) {
   if (!c) return FCG_OK;
+  for (auto& v : c->alias_segs)
+    for (int32_t g : v) --c->alias_lib->segs[g].pins;
   if (!c->layout_only()) {
     hipSetDevice(c->device);
     hipDeviceSynchronize();
@@ -620,9 +786,16 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   if (n_items == 0) return FCG_OK;
   if (c->plan.alias_v() && c->alias_lib && c->alias_lib != lib)
     return fail(FCG_EINVAL, "a cache with FCG_ALIAS_V grafts from one library only");
+  for (auto& sp : spans)
+    if (lib->segs[sp.seg].tok_off < 0) return fail(FCG_ESTATE, "segment is not in device memory (fcg_lib_reload)");
   if (c->plan.alias_v()) {
     c->alias_lib = lib;
-    for (auto& sp : spans) c->plan.alias_pages(sp.seq, sp.dst, sp.len, lib->segs[sp.seg].tok_off);
+    if (c->alias_segs.empty()) c->alias_segs.resize(c->n_seqs);
+    for (auto& sp : spans) {
+      c->plan.alias_pages(sp.seq, sp.dst, sp.len, lib->segs[sp.seg].tok_off);
+      ++lib->segs[sp.seg].pins;  // its values may now be read in place: no offload until the sequence is reset
+      c->alias_segs[sp.seq].push_back(sp.seg);
+    }
   }
   if (c->layout_only()) {
     c->plan.map_pages(new_pages);

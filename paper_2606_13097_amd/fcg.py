@@ -33,6 +33,7 @@ FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE,
 # every symbol include/fcg.h declares
 EXPORTS = [
     "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
+    "fcg_lib_host_reserve", "fcg_lib_offload", "fcg_lib_reload", "fcg_lib_segment_state",
     "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_export_v_alias",
     "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
@@ -72,6 +73,10 @@ def _load():
         "fcg_lib_segment_info": [P, I32, PI64, PI32, PI32],
         "fcg_lib_device_ptrs": [P, I32, C.POINTER(P), C.POINTER(P)],
         "fcg_lib_destroy": [P],
+        "fcg_lib_host_reserve": [P, I64],
+        "fcg_lib_offload": [P, I32, P],
+        "fcg_lib_reload": [P, I32, P],
+        "fcg_lib_segment_state": [P, I32, PI32, PI32],
         "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
         "fcg_cache_reset": [P, I32],
         "fcg_cache_truncate": [P, I32, I32, P],
@@ -214,6 +219,25 @@ def fcg_lib_device_ptrs(lib: Library, layer: int):
 
 def fcg_lib_destroy(lib: Library) -> None:
     lib.close()
+
+
+def fcg_lib_host_reserve(lib: Library, host_tokens: int) -> None:
+    _check(_L.fcg_lib_host_reserve(lib.h, int(host_tokens)))
+
+
+def fcg_lib_offload(lib: Library, seg: int, stream=None) -> None:
+    _check(_L.fcg_lib_offload(lib.h, int(seg), _stream(stream)))
+
+
+def fcg_lib_reload(lib: Library, seg: int, stream=None) -> None:
+    _check(_L.fcg_lib_reload(lib.h, int(seg), _stream(stream)))
+
+
+def fcg_lib_segment_state(lib: Library, seg: int):
+    """-> (in device memory, has a host copy)."""
+    a, b = C.c_int32(), C.c_int32()
+    _check(_L.fcg_lib_segment_state(lib.h, int(seg), C.byref(a), C.byref(b)))
+    return bool(a.value), bool(b.value)
 
 
 def fcg_cache_create(desc: ModelDesc, n_seqs: int, max_tokens: int, page_size: int = 0, n_pages: int = 0,

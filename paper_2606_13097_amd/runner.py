@@ -24,14 +24,15 @@ TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
 
 
 class GpuSetup:
-    def __init__(self, w: synth.Workload, device: str = "cuda", n_caches: int = 1, cache_flags: int = 0):
+    def __init__(self, w: synth.Workload, device: str = "cuda", n_caches: int = 1, cache_flags: int = 0,
+                 lib_spare_tokens: int = 0):
         self.w = w
         sh = w.shape
         self.desc = fcg.model_desc(sh.n_layers, sh.n_q_heads, sh.n_kv_heads, sh.head_dim, sh.rope_theta, sh.dtype)
         self.device = device
         self.tdtype = TORCH_DTYPE[sh.dtype]
-        cap = int(w.lib_lengths.sum())
-        self.lib = fcg.Library(self.desc, cap, len(w.lib_lengths))
+        cap = int(w.lib_lengths.sum()) + int(lib_spare_tokens)
+        self.lib = fcg.Library(self.desc, cap, len(w.lib_lengths) + (8 if lib_spare_tokens else 0))
         self._fill_library()
         self.caches = [fcg.Cache(self.desc, w.n_seqs, w.max_tokens, w.page_size, w.n_pages, flags=cache_flags)
                        for _ in range(n_caches)]

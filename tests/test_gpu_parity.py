@@ -458,3 +458,41 @@ def test_cache_patching_cut_regenerate_decode(dtype, page, alias):
         say("[gpu]   patch parity ok")
     finally:
         setup.close()
+
+
+@pytest.mark.gpu
+def test_offload_reload_round_trip_is_bit_exact():
+    """Segments offloaded to the pinned host tier and reloaded at other device offsets
+    (a new segment took their old range) graft exactly as before: every grafted key and
+    value of the cache is bit-identical to the first graft's."""
+    from paper_2606_13097_amd import fcg, runner
+    w = synth.workload("7b", seed=5, n_layers=2, n_lib=12)
+    segs = sorted(set(int(g) for g in w.graft_seg))
+    spare = int(sum(int(w.lib_lengths[g]) for g in segs))   # room to reload every one past the others
+    say(f"[gpu] offload/reload segs={segs}")
+    setup = runner.GpuSetup(w, lib_spare_tokens=spare)
+    try:
+        fcg.fcg_lib_host_reserve(setup.lib, int(w.lib_lengths.sum()))
+        setup.graft()
+        pos = np.flatnonzero(fcg.fcg_cache_export_layout(setup.cache, 0, 0)[2])
+        ref = [read_cache(setup.cache, w, layer, 0, pos) for layer in range(2)]
+        before = {g: fcg.fcg_lib_segment_info(setup.lib, g)[0] for g in segs}
+        for g in segs:
+            fcg.fcg_lib_offload(setup.lib, g)
+        # a new segment as long as the first offloaded one takes the lowest freed range
+        fcg.fcg_lib_add_segment(setup.lib, int(w.lib_lengths[segs[0]]), 0)
+        for g in reversed(segs):
+            fcg.fcg_lib_reload(setup.lib, g)
+        after = {g: fcg.fcg_lib_segment_info(setup.lib, g)[0] for g in segs}
+        assert any(after[g] != before[g] for g in segs), (before, after)
+        assert all(fcg.fcg_lib_segment_state(setup.lib, g) == (True, True) for g in segs)
+        setup.reset()
+        setup.graft()
+        torch.cuda.synchronize()
+        for layer in range(2):
+            gk, gv = read_cache(setup.cache, w, layer, 0, pos)
+            np.testing.assert_array_equal(gk, ref[layer][0])
+            np.testing.assert_array_equal(gv, ref[layer][1])
+        say("[gpu]   round trip bit-exact")
+    finally:
+        setup.close()
