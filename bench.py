@@ -444,7 +444,9 @@ def main():
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},
     }
     res["locality"] = locality_update(w, task_ws)
-    # host tier: one task's segments to pinned host memory and back
+    # host tier: one task's segments to pinned host memory and back (the cache
+    # is emptied first: a value-aliasing cache pins the segments it reads)
+    setup.reset()
     segs = sorted(set(int(g) for g in task_ws[0].graft_seg))
     tokens = sum(int(w.lib_lengths[g]) for g in segs)
     fcg.fcg_lib_host_reserve(lib, tokens)
