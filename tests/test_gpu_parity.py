@@ -332,6 +332,7 @@ def test_kernel_timing_counts_calls():
 
 @pytest.mark.gpu
 @pytest.mark.parametrize("hq,hkv,d,dtype", [(32, 8, 128, "bf16"), (64, 8, 128, "bf16"), (8, 4, 64, "bf16"),
+                                            (4, 4, 128, "bf16"), (16, 1, 64, "bf16"),
                                             (4, 2, 64, "f32")])
 def test_decode_split_edges(hq, hkv, d, dtype):
     """Decode positions on and next to the 64-key split boundaries (a last split holding only
