@@ -75,6 +75,10 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
   constexpr int VPT = (STAGE * VB + NT - 1) / NT;   // staged V blocks per lane
   using Tile = PrefillTile<D>;
   __shared__ Tile tiles[STAGE];
+  // paged caches: the split's page and value-alias entries, read into LDS once
+  // (a table lookup per row would put a dependent load before every round's loads)
+  constexpr int NPG = PAGED ? kPageWindow : 1;
+  __shared__ int32_t s_pg[NPG], s_al[NPG];
 
   const PrefillRb rb = args.rb[blockIdx.x];
   const int split = blockIdx.y;
@@ -95,6 +99,17 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
   if (k0 >= kend) return;  // padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
+  const int lpa = k0 >> 4;
+  const int npg = PAGED ? ((kend - 1) >> 4) - lpa + 1 : 0;
+  const bool window = PAGED && npg <= NPG;  // else: entries read from memory per row (block-uniform)
+  if (window) {
+    const int32_t* row = cv.page_table + (int64_t)rb.seq * 2 * cv.n_lp + lpa;
+    for (int e = t; e < npg; e += NT) {
+      s_pg[e] = row[e];
+      s_al[e] = cv.v_alias ? row[cv.n_lp + e] : -1;
+    }
+    __syncthreads();
+  }
   const int w = t >> 6, lane = t & 63;
   const int lr = lane & 15, lq = lane >> 4;
   const int rows = rb.n_rank * g;
@@ -120,11 +135,25 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
   const int64_t head_base = PAGED ? 0 : kv_offset<false>(cv, layer, rb.seq, hk, 0);
   const bf16_t* kbase = ck + head_base;
   const bf16_t* vbase = cvv + head_base;
+  // rows of positions in [k0, kend)
   auto krow = [&](int p) -> const bf16_t* {
-    return PAGED ? ck + kv_offset<true>(cv, layer, rb.seq, hk, p) : kbase + p * D;
+    if (!PAGED) return kbase + p * D;
+    if (window)
+      return ck + (int64_t)layer * cv.layer_stride +
+             (((int64_t)s_pg[(p >> 4) - lpa] * Hkv + hk) * 16 + (p & 15)) * D;
+    return ck + kv_offset<true>(cv, layer, rb.seq, hk, p);
   };
   auto vrow = [&](int p) -> const bf16_t* {
-    return PAGED ? v_row<true, bf16_t>(cv, layer, rb.seq, hk, p) : vbase + p * D;
+    if (!PAGED) return vbase + p * D;
+    if (window) {
+      const int e = (p >> 4) - lpa;
+      const int32_t a = s_al[e];
+      if (a >= 0)
+        return reinterpret_cast<const bf16_t*>(cv.lib_v) +
+               (((int64_t)layer * Hkv + hk) * cv.lib_cap + a + (p & 15)) * D;
+      return cvv + (int64_t)layer * cv.layer_stride + (((int64_t)s_pg[e] * Hkv + hk) * 16 + (p & 15)) * D;
+    }
+    return v_row<true, bf16_t>(cv, layer, rb.seq, hk, p);
   };
 
   float mrow[2] = {-INFINITY, -INFINITY};

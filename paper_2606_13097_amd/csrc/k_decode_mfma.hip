@@ -74,6 +74,10 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   __shared__ float s_mt[NSL * G], s_lt[NSL * G];
   __shared__ __align__(16) bf16_t s_newk[D], s_newv[D];  // the new token's encoded key and value
   __shared__ int s_last;
+  // paged caches: the split's page and value-alias entries, read into LDS once
+  // (a table lookup per tile would put a dependent load before every tile's loads)
+  constexpr int NPG = PAGED ? kPageWindow : 1;
+  __shared__ int32_t s_pg[NPG], s_al[NPG];
 
   const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
   const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
@@ -99,6 +103,19 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   const int kend = owns_new ? pos : k1;  // cached keys [k0, kend)
   const int ntile = (kend - k0 + 15) >> 4;
 
+  // pages holding [ka, kend), ka = the lowest position a (clamped) load reads
+  const int ka = max(0, min(k0, kend - 1));
+  const int lpa = ka >> 4;
+  const int npg = PAGED ? (max(ka, kend - 1) >> 4) - lpa + 1 : 0;
+  const bool window = PAGED && npg <= NPG;  // else: entries read from memory per load (block-uniform)
+  if (window) {
+    const int32_t* row = cv.page_table + (int64_t)seq * 2 * cv.n_lp + lpa;
+    for (int e = t; e < npg; e += 256) {
+      s_pg[e] = row[e];
+      s_al[e] = cv.v_alias ? row[cv.n_lp + e] : -1;
+    }
+  }
+
   // ---- loads, in the order their data is needed
   const double wfreq = inv_freq[t % HALF];
   uint4 qa[KS], qb[KS];  // query head lr (row g - 1 for columns past the group): dims and rotary partners
@@ -122,18 +139,34 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
     nb = ld16(krow + (dn < HALF ? dn + HALF : dn - HALF));
     nv = ld16(vrow + dn);
   }
+  // key and value rows of cached position p (p in [ka, kend))
+  auto k_ptr = [&](int p) -> const bf16_t* {
+    if (window) {
+      const int32_t page = s_pg[(p >> 4) - lpa];
+      return ck + (int64_t)layer * cv.layer_stride + (((int64_t)page * Hkv + hk) * 16 + (p & 15)) * D;
+    }
+    return ck + kv_offset<PAGED>(cv, layer, seq, hk, p);
+  };
+  auto v_ptr = [&](int p) -> const bf16_t* {
+    if (window) {
+      const int e = (p >> 4) - lpa;
+      const int32_t a = s_al[e];
+      if (a >= 0)
+        return reinterpret_cast<const bf16_t*>(cv.lib_v) +
+               (((int64_t)layer * Hkv + hk) * cv.lib_cap + a + (p & 15)) * D;
+      return cvv + (int64_t)layer * cv.layer_stride + (((int64_t)s_pg[e] * Hkv + hk) * 16 + (p & 15)) * D;
+    }
+    return v_row<PAGED, bf16_t>(cv, layer, seq, hk, p);
+  };
+  if (window) __syncthreads();  // the page window is in LDS (a block-uniform branch)
   // a tile's keys (A layout) and V block; keys past the range re-read the last key
   auto load_tile = [&](int ti, uint4 (&kk)[KS], uint4 (&vv)[4]) {
     const int kb = k0 + ti * 16;
-    const int pk = max(0, min(kb + lr, kend - 1));
-    const int64_t ko = kv_offset<PAGED>(cv, layer, seq, hk, pk) + lq * 8;
+    const bf16_t* kr = k_ptr(max(0, min(kb + lr, kend - 1))) + lq * 8;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) kk[ks] = ld16(ck + ko + ks * 32);
+    for (int ks = 0; ks < KS; ++ks) kk[ks] = ld16(kr + ks * 32);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int pv = max(0, min(kb + 4 * kg + r, kend - 1));
-      vv[r] = ld16(v_row<PAGED, bf16_t>(cv, layer, seq, hk, pv) + dg * 8);
-    }
+    for (int r = 0; r < 4; ++r) vv[r] = ld16(v_ptr(max(0, min(kb + 4 * kg + r, kend - 1))) + dg * 8);
   };
   uint4 kA[KS], vA[4], kB[KS], vB[4], kC[KS], vC[4];
   load_tile(w, kA, vA);

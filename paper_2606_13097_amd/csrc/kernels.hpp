@@ -62,6 +62,10 @@ __device__ __forceinline__ int64_t kv_offset(const CacheView& c, int layer, int 
   return (int64_t)layer * c.layer_stride + (((int64_t)seq * c.n_kv_heads + head) * c.max_tokens + pos) * c.head_dim;
 }
 
+// Pages of a paged cache whose entries a block stages in LDS (the page window
+// of its key range); a longer range reads the entries from memory.
+constexpr int kPageWindow = 520;
+
 // Value row (layer, seq, head, pos) to read: the cache's own row, or the
 // library's row for a page whose values are mapped onto the library.
 template <bool PAGED, typename T>
