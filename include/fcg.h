@@ -15,7 +15,8 @@
  *  - Every entry point returns an fcg_status; nothing aborts or throws across
  *    the ABI.  fcg_last_error() gives a thread-local message for the last
  *    failing call on the calling thread.
- *  - A call that returns an error changes no state.
+ *  - A call that returns an error changes no state (an EHIP failure of the
+ *    runtime after a call's checks aside).
  *  - "device" pointers are HIP device memory on the current device; "host"
  *    pointers are ordinary host memory, read (or written) before the call
  *    returns.  The caller keeps ownership of everything it passes.
@@ -51,7 +52,7 @@ typedef enum {
   FCG_ERANGE = 2,   /* index out of range: layer, sequence, segment, position, span end */
   FCG_EOVERLAP = 3, /* a target position is given twice or is already written */
   FCG_EHOLE = 4,    /* attention would read a position that is not written */
-  FCG_ENOMEM = 5,   /* device memory, library capacity or page pool exhausted */
+  FCG_ENOMEM = 5,   /* device memory, library capacity, host tier or page pool exhausted */
   FCG_ESTATE = 6,   /* operation not valid in the current state (e.g. decode on an empty sequence) */
   FCG_EHIP = 7      /* the HIP runtime reported an error */
 } fcg_status;
@@ -63,7 +64,7 @@ typedef enum { FCG_F32 = 0, FCG_BF16 = 1 } fcg_dtype;
  * together by p * theta^(-2i/D) at position p (rope_style 0, the only one). */
 typedef struct {
   int32_t n_layers;   /* L >= 1 */
-  int32_t n_q_heads;  /* Hq, a multiple of Hkv; Hq / Hkv <= 16 */
+  int32_t n_q_heads;  /* Hq, with Hq / Hkv one of 1, 2, 4, 8, 16 */
   int32_t n_kv_heads; /* Hkv >= 1 */
   int32_t head_dim;   /* D: 64 or 128 */
   double rope_theta;  /* theta > 1 */
