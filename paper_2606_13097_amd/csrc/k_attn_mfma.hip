@@ -348,11 +348,13 @@ int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void*
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
-  const bool stage4 = args.span > 2 * kBN;      // splits of more than two tiles stage four per round
+  // tiles staged per round: the split's tile count up to four (a slot past the
+  // round's last tile repeats that tile's loads)
+  const int stage = args.span <= 2 * kBN ? 2 : args.span <= 3 * kBN ? 3 : 4;
 #define PF(DD, PG, WV, ST)                                                                                  \
   hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, ST>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta,     \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFS(DD, PG, WV) { if (stage4) PF(DD, PG, WV, 4); else PF(DD, PG, WV, 2); }
+#define PFS(DD, PG, WV) { if (stage == 4) PF(DD, PG, WV, 4); else if (stage == 3) PF(DD, PG, WV, 3); else PF(DD, PG, WV, 2); }
 #define PFW(DD, PG) { if (waves == 8) PFS(DD, PG, 8) else PFS(DD, PG, 4) }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
