@@ -8,19 +8,21 @@
 // split [k0, k1) of the key positions.  Wave w owns rows 32w .. 32w + 31 as
 // two 16-row tiles.
 //
-// The block stages 2 or 4 tiles of 64 keys at once: every load of the round
-// is issued before any LDS write (one memory latency per round instead of one
-// per tile), K as rows [key][D], V transposed [d][key] (each lane transposes
-// 4-key x 8-dim blocks in registers with v_perm).  Then per tile, with no
-// barrier:
+// Key tiles of 64 keys go from memory straight into LDS (global_load_lds:
+// each instruction fills 1 KB, 16 bytes per lane), into a ring of four
+// single-tile buffers, so three tiles are in flight while one is attended and
+// staging costs no registers.  K and V keep their [key][D] rows; the 16-byte
+// chunks of each row are XOR-swizzled so that the reads below meet no bank
+// conflicts.  Then per tile:
 //   - S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K from LDS, B = Q^T held
 //     in registers for the whole block).  In the accumulator layout lane l
 //     holds keys 4(l/16) .. +3 of a 16-key tile for query row l % 16, so each
 //     lane owns one query row: the running max needs only two cross-lane
 //     exchanges (lanes l ^ 16, l ^ 32) and the running sum none until the end.
-//   - O^T += V^T P^T (A = V^T from LDS, B = P^T straight from the S^T
-//     registers rounded to bf16: the k index of the two 16-key tiles that
-//     make one 32-deep step is the same permutation in A and B).
+//   - O^T += V^T P^T (A = V^T read from the V rows with the LDS transpose read
+//     ds_read_b64_tr_b16, B = P^T straight from the S^T registers rounded to
+//     bf16: the k index of the two 16-key tiles that make one 32-deep step is
+//     the same permutation in A and B).
 // The causal mask is by position: key p is visible to a row at position q iff
 // p <= q.  A block covering a row block's whole range writes the normalised
 // output; otherwise a partial (max, sum, unnormalised output) for the combine.
@@ -46,37 +48,68 @@ __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, 
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(a), as_bf16x8(b), c, 0, 0, 0);
 }
 
-constexpr int kBN = 64;  // keys per tile
+constexpr int kBN = 64;    // keys per tile
+constexpr int kNBuf = 4;   // tiles in the LDS ring: three in flight while one is attended
 
 template <int D>
 struct PrefillTile {
-  // Row pitches chosen for conflict-free LDS reads: a 16-byte K read by 8
-  // lanes of 8 rows covers banks 4r .. 4r + 3 (pitch 68 dwords), an 8-byte
-  // V^T read by 16 lanes of 16 rows covers banks 2r, 2r + 1 (pitch 34 dwords).
-  static constexpr int KROW = D + 8;     // bf16 elements per staged K row
-  static constexpr int VROW = kBN + 4;   // bf16 elements per staged V^T row
-  bf16_t k[kBN * KROW];
-  bf16_t vt[D * VROW];
+  // [key][D] rows, 16-byte chunk c of row r at chunk position c ^ swz(r):
+  //  - K is read as MFMA A fragments, 16 bytes per lane from 16 rows x 4
+  //    chunks: swz_k(r) = r % NC puts every 8 (and every 16) lanes' reads in
+  //    distinct banks;
+  //  - V is read with ds_read_b64_tr_b16, 8 bytes per lane from 4 rows x 2
+  //    chunks per 16 lanes: swz_v(r) = 2 (r % (NC / 2)) does the same.
+  static constexpr int NC = D / 8;  // 16-byte chunks per row
+  bf16_t k[kBN * D];
+  bf16_t v[kBN * D];
+  __device__ static int swz_k(int r) { return r % NC; }
+  __device__ static int swz_v(int r) { return 2 * (r % (NC / 2)); }
 };
 
-// grid (row block, key split, kv head); STAGE tiles of the split are staged
-// per round
-template <int D, bool PAGED, int WAVES, int STAGE>
-__global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kernel(
+// LDS byte address of a pointer into a __shared__ array
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)p;
+}
+// global -> LDS, 16 bytes per lane: lane l's bytes land at lds + 16 l (lds
+// wave-uniform).  Inline assembly, so that the compiler's own wait
+// bookkeeping, which cannot tell the ring's buffers apart, adds no
+// vmcnt(0) before each tile's LDS reads; the waits are explicit (wait_vm).
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
+}
+// s_waitcnt vmcnt(N): at most N of this wave's vector memory operations remain
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+}
+// this wave's LDS reads have returned, then the workgroup barrier
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+// ds_read_b64_tr_b16: within each 16-lane group, lane j receives element j % 4
+// of the 8 bytes addressed by lanes 4e + j / 4, e = 0..3
+__device__ __forceinline__ uint2 ld_tr8(const bf16_t* p) {
+  const i16x4_t x = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4_t*)(const_cast<bf16_t*>(p)));
+  return __builtin_bit_cast(uint2, x);
+}
+
+// grid (row block, key split, kv head)
+template <int D, bool PAGED, int WAVES>
+__global__ void __launch_bounds__(WAVES * 64, 1) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int part_stride_rows) {
   constexpr int NT = WAVES * 64;                    // lanes per block
   constexpr int KS = D / 32;                        // 32-deep k steps over the head dimension
   constexpr int DT = D / 16;                        // 16-wide output tiles over the head dimension
-  constexpr int KV = kBN * D / 8;                   // 16-byte K vectors per tile
-  constexpr int VB = (kBN / 4) * (D / 8);           // 4-key x 8-dim V blocks per tile
-  constexpr int KPT = (STAGE * KV + NT - 1) / NT;   // staged K vectors per lane
-  constexpr int VPT = (STAGE * VB + NT - 1) / NT;   // staged V blocks per lane
   using Tile = PrefillTile<D>;
-  __shared__ Tile tiles[STAGE];
+  constexpr int NC = Tile::NC;
+  constexpr int DPT = 2 * NC / WAVES;               // LDS loads per wave per tile (1 KB each)
+  static_assert(NC % WAVES == 0, "tile loads split evenly over the waves");
+  __shared__ Tile tiles[kNBuf];
   // paged caches: the split's page and value-alias entries, read into LDS once
-  // (a table lookup per row would put a dependent load before every round's loads)
+  // (a table lookup per row would put a dependent load before every tile's loads)
   constexpr int NPG = PAGED ? kPageWindow : 1;
   __shared__ int32_t s_pg[NPG], s_al[NPG];
 
@@ -111,6 +144,7 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
     __syncthreads();
   }
   const int w = t >> 6, lane = t & 63;
+  const int wu = __builtin_amdgcn_readfirstlane(w);  // the wave index, in a scalar register
   const int lr = lane & 15, lq = lane >> 4;
   const int rows = rb.n_rank * g;
   const float qscale = 1.4426950408889634f / sqrtf((float)D);
@@ -155,7 +189,27 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
     }
     return v_row<true, bf16_t>(cv, layer, rb.seq, hk, p);
   };
-
+  // This wave's share of tile `tile` into its ring buffer: instruction j of
+  // the tile (K: 0 .. NC - 1, V: NC .. 2 NC - 1) fills slots 64 j' .. 64 j' + 63
+  // of the K or V rows, lane l the slot of row (64 j' + l) / NC at chunk
+  // position (64 j' + l) % NC, so it loads the chunk that the swizzle puts
+  // there.  Keys past the split read its last key (valid memory; masked).
+  const int ntiles = (kend - k0 + kBN - 1) / kBN;
+  auto issue = [&](int tile) {
+    Tile& B = tiles[tile % kNBuf];
+    const int kb = k0 + tile * kBN;
+#pragma unroll
+    for (int u = 0; u < DPT; ++u) {
+      const bool isv = WAVES * u >= NC;  // compile-time: instructions u < NC / WAVES are K
+      const int jj = wu + WAVES * u - (isv ? NC : 0);
+      const int slot = jj * 64 + lane;
+      const int r = slot / NC, pos = slot % NC;
+      const int p = min(kb + r, kend - 1);
+      const int c = pos ^ (isv ? Tile::swz_v(r) : Tile::swz_k(r));
+      const bf16_t* src = (isv ? vrow(p) : krow(p)) + c * 8;
+      dma16(src, lds_addr(isv ? B.v : B.k) + jj * 1024);
+    }
+  };
   float mrow[2] = {-INFINITY, -INFINITY};
   float lsum[2] = {0.f, 0.f};
   floatx4 acc[2][DT];
@@ -164,61 +218,45 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kr0 = k0; kr0 < kend; kr0 += STAGE * kBN) {
-    const int nt = min(STAGE, (kend - kr0 + kBN - 1) / kBN);  // tiles of this round
-    // ---- issue every load of the round, then stage it.  Loads and LDS
-    // writes are unconditional: slots past the round's last tile repeat that
-    // tile (the same bytes to the same LDS addresses), and positions past the
-    // split are clamped to its last key (valid memory, scores masked).  A
-    // conditional load would make the compiler wait, in the next round, for
-    // loads it cannot prove complete before reusing their registers.
-    uint4 kreg[KPT], vreg[VPT][4];
+  // Prologue: the first kNBuf - 1 tiles go in flight.  The query rows and
+  // metadata were loaded before them; the empty asm makes the compiler wait
+  // for those loads here (it waits for every vector load, these tiles
+  // included), not inside the loop, where its wait would also drain the
+  // prefetched tiles on every pass.
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int idx = i * NT + t;  // (tile, key, 16-byte chunk)
-      const int tl = min(idx / KV, nt - 1), key = (idx % KV) / (D / 8), c = idx % (D / 8);
-      kreg[i] = ld16(krow(min(kr0 + tl * kBN + key, kend - 1)) + c * 8);
-    }
+  for (int i = 0; i < kNBuf - 1; ++i)
+    if (i < ntiles) issue(i);
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int idx = i * NT + t;  // (tile, 4-key group, 8-dim chunk)
-      const int tl = min(idx / VB, nt - 1), kg = idx % 16, dc = (idx % VB) / 16;
+  for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) vreg[i][j] = ld16(vrow(min(kr0 + tl * kBN + kg * 4 + j, kend - 1)) + dc * 8);
-    }
-    if (kr0 != k0) __syncthreads();  // the previous round's tiles are no longer read
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int idx = i * NT + t;
-      const int tl = min(idx / KV, nt - 1), key = (idx % KV) / (D / 8), c = idx % (D / 8);
-      st16(&tiles[tl].k[key * Tile::KROW + c * 8], kreg[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int idx = i * NT + t;
-      const int tl = min(idx / VB, nt - 1), kg = idx % 16, dc = (idx % VB) / 16;
-      // vreg[i][j] = V[key 4kg + j][dims 8dc .. +7]; transposed row e = V[4kg .. 4kg + 3][8dc + e]
-      const uint32_t* x = reinterpret_cast<const uint32_t*>(vreg[i]);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
-        const uint32_t w01 = __builtin_amdgcn_perm(x[4 + e / 2], x[e / 2], sel);
-        const uint32_t w23 = __builtin_amdgcn_perm(x[12 + e / 2], x[8 + e / 2], sel);
-        *reinterpret_cast<uint2*>(&tiles[tl].vt[(dc * 8 + e) * Tile::VROW + kg * 4]) = make_uint2(w01, w23);
-      }
-    }
-    __syncthreads();
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(__builtin_bit_cast(u32x4_t, qf[rt][ks])));
+    asm volatile("" ::"v"(rpos[rt]), "v"(rtok[rt]));
+  }
 
-    for (int tl = 0; tl < nt; ++tl) {
-      const Tile& T = tiles[tl];
-      const int kb = kr0 + tl * kBN;
+  for (int tile = 0; tile < ntiles; ++tile) {
+    // this wave's loads of the tile have landed (the later tiles in flight,
+    // up to kNBuf - 2 of them, may still be pending) ...
+    const int ahead = min(kNBuf - 2, ntiles - 1 - tile);
+    if (ahead >= 2) wait_vm<2 * DPT>();
+    else if (ahead == 1) wait_vm<DPT>();
+    else wait_vm<0>();
+    // ... and every wave's; every wave is also done with the previous tile,
+    // whose buffer the next load reuses
+    lds_barrier();
+    if (tile + kNBuf - 1 < ntiles) issue(tile + kNBuf - 1);
+    {
+      const Tile& T = tiles[tile % kNBuf];
+      const int kb = k0 + tile * kBN;
       // S^T = K Q^T: four 16-key tiles x two 16-row tiles
       floatx4 st[2][4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         uint4 ka[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) ka[ks] = ld16(&T.k[(kt * 16 + lr) * Tile::KROW + ks * 32 + lq * 8]);
+        for (int ks = 0; ks < KS; ++ks) {
+          const int r = kt * 16 + lr;
+          ka[ks] = ld16(&T.k[(r * NC + ((ks * 4 + lq) ^ Tile::swz_k(r))) * 8]);
+        }
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
           floatx4 c = {0.f, 0.f, 0.f, 0.f};
@@ -288,14 +326,20 @@ __global__ void __launch_bounds__(WAVES * 64, 8 / WAVES) attn_prefill_mfma_kerne
                                  cvt_bf16x2(pv[2 * s + 1][0], pv[2 * s + 1][1]),
                                  cvt_bf16x2(pv[2 * s + 1][2], pv[2 * s + 1][3]));
       }
-      // O^T += V^T P^T
+      // O^T += V^T P^T.  A fragment of step s, dims 16 dt ..: lane (lr, lq)
+      // needs V[32 s + 4 lq + e][16 dt + lr] (e = 0..3) and the same 16 keys
+      // later; in the transpose read, lane lr of group lq addresses row
+      // 32 s + 4 lq + lr / 4 (+ 16), dims 16 dt + 4 (lr % 4) .. + 3.
+      const int vr = 4 * lq + (lr >> 2);                 // row within a 32-key step
+      const int vsw = Tile::swz_v(vr);                   // the same for rows vr + 16, + 32, + 48
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
+        const int vc = (2 * dt + ((lr & 3) >> 1)) ^ vsw;  // chunk position of dims 16 dt + 4 (lr % 4)
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
-          const bf16_t* row = &T.vt[(dt * 16 + lr) * Tile::VROW + s * 32 + lq * 4];
-          const uint2 lo = *reinterpret_cast<const uint2*>(row);
-          const uint2 hi = *reinterpret_cast<const uint2*>(row + 16);
+          const bf16_t* row = &T.v[((32 * s + vr) * NC + vc) * 8 + (lr & 1) * 4];
+          const uint2 lo = ld_tr8(row);
+          const uint2 hi = ld_tr8(row + 16 * D);
           const uint4 va = make_uint4(lo.x, lo.y, hi.x, hi.y);
 #pragma unroll
           for (int rt = 0; rt < 2; ++rt) acc[rt][dt] = mfma16x16x32(va, pb[rt][s], acc[rt][dt]);
@@ -348,19 +392,14 @@ int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void*
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
-  // tiles staged per round: the split's tile count up to four (a slot past the
-  // round's last tile repeats that tile's loads)
-  const int stage = args.span <= 2 * kBN ? 2 : args.span <= 3 * kBN ? 3 : 4;
-#define PF(DD, PG, WV, ST)                                                                                  \
-  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, ST>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta,     \
+#define PF(DD, PG, WV)                                                                                      \
+  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta,     \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFS(DD, PG, WV) { if (stage == 4) PF(DD, PG, WV, 4); else if (stage == 3) PF(DD, PG, WV, 3); else PF(DD, PG, WV, 2); }
-#define PFW(DD, PG) { if (waves == 8) PFS(DD, PG, 8) else PFS(DD, PG, 4) }
+#define PFW(DD, PG) { if (waves == 8) PF(DD, PG, 8); else PF(DD, PG, 4); }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
   else { if (paged) PFW(64, true) else PFW(64, false) }
 #undef PFW
-#undef PFS
 #undef PF
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
