@@ -841,18 +841,28 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   const int n = (int)meta.size();
   const int g = d.n_q_heads / d.n_kv_heads;
   const bool mfma = d.dtype == FCG_BF16;
-  // row blocks: consecutive ranks of one sequence, at most 256 query rows (MFMA) or one token
-  const int max_rank = mfma ? std::max(1, 256 / g) : 1;
-  std::vector<std::pair<int, int>> rblocks;  // (rank0, n_rank)
-  for (int r = 0; r < n;) {
-    int u = r;
-    while (u < n && meta[u].seq == meta[r].seq && u - r < max_rank) ++u;
-    rblocks.push_back({r, u - r});
-    r = u;
-  }
+  // row blocks: consecutive ranks of one sequence, at most 256 (or 128) query
+  // rows (MFMA) or one token
+  auto row_blocks = [&](int max_rank) {
+    std::vector<std::pair<int, int>> rb;  // (rank0, n_rank)
+    for (int r = 0; r < n;) {
+      int u = r;
+      while (u < n && meta[u].seq == meta[r].seq && u - r < max_rank) ++u;
+      rb.push_back({r, u - r});
+      r = u;
+    }
+    return rb;
+  };
+  std::vector<std::pair<int, int>> rblocks = row_blocks(mfma ? std::max(1, 256 / g) : 1);
+  // MFMA: unless 256-row blocks alone fill the chip twice, use 128-row blocks
+  // of 4 waves sized to run two per CU (one block's softmax beside the other's
+  // matrix work), with the key splits planned for 512 blocks
+  const bool pair = mfma && (int64_t)rblocks.size() * d.n_kv_heads < 512;
+  if (pair) rblocks = row_blocks(std::max(1, 128 / g));
   // split the key range of each row block so that the grid covers the chip
   // once: one split length (in tiles) for the call, the smallest whose blocks
-  // fit one per CU; at most 256 splits per row block (the merge table)
+  // fit one per CU (two in pair mode); at most 256 splits per row block (the
+  // merge table)
   const int tile = mfma ? 64 : 256;
   std::vector<int64_t> rb_tiles;
   int64_t total_tiles = 0, max_tiles = 0;
@@ -861,7 +871,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     total_tiles += rb_tiles.back();
     max_tiles = std::max(max_tiles, rb_tiles.back());
   }
-  const int64_t target = 256;
+  const int64_t target = pair ? 512 : 256;
   const int min_tiles = mfma ? 2 : 1;
   int64_t per = std::max<int64_t>({(int64_t)min_tiles, (total_tiles * d.n_kv_heads + target - 1) / target,
                                    (max_tiles + 255) / 256});
@@ -909,7 +919,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   // MFMA blocks of 8 waves (256 rows) when some row block needs more than 4 waves
   int max_rows = 0;
   for (auto& rb : rblocks) max_rows = std::max(max_rows, rb.second * g);
-  const int stride_rows = mfma ? (max_rows > 128 ? 256 : 128) : g;
+  const int stride_rows = mfma ? (max_rows > 128 ? 256 : 128) : g;  // pair: max_rows <= 128
   // workspaces first: a failure here leaves the layout untouched
   const size_t qbytes = (size_t)d.n_kv_heads * n * g * d.head_dim * esize(d.dtype);
   if (fcg_status st = grow(&c->qws, &c->qws_bytes, qbytes, "query workspace")) return st;
@@ -940,7 +950,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     for (size_t li = 0; li < pf_launch.size(); ++li) {
       const KTime tm{li == 0 ? e_attn0 : nullptr, li + 1 == pf_launch.size() ? e_attn1 : nullptr};
       rc = launch_attn_mfma(pf_launch[li], dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml,
-                            stride_rows, s, tm);
+                            stride_rows, pair, s, tm);
       if (rc) break;
     }
   } else

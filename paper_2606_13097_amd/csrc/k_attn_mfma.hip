@@ -49,7 +49,6 @@ __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, 
 }
 
 constexpr int kBN = 64;    // keys per tile
-constexpr int kNBuf = 4;   // tiles in the LDS ring: three in flight while one is attended
 
 template <int D>
 struct PrefillTile {
@@ -94,9 +93,12 @@ __device__ __forceinline__ uint2 ld_tr8(const bf16_t* p) {
   return __builtin_bit_cast(uint2, x);
 }
 
-// grid (row block, key split, kv head)
-template <int D, bool PAGED, int WAVES>
-__global__ void __launch_bounds__(WAVES * 64, 1) attn_prefill_mfma_kernel(
+// grid (row block, key split, kv head).  NBUF tiles in the LDS ring: 4 (three
+// in flight while one is attended) for one block per CU, 2 (132 KB against
+// 68 KB of LDS at D 128) for two 4-wave blocks per CU, whose phases then
+// overlap (one block's softmax beside the other's matrix work).
+template <int D, bool PAGED, int WAVES, int NBUF>
+__global__ void __launch_bounds__(WAVES * 64, NBUF == 2 ? 2 : 1) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int part_stride_rows) {
@@ -107,6 +109,7 @@ __global__ void __launch_bounds__(WAVES * 64, 1) attn_prefill_mfma_kernel(
   constexpr int NC = Tile::NC;
   constexpr int DPT = 2 * NC / WAVES;               // LDS loads per wave per tile (1 KB each)
   static_assert(NC % WAVES == 0, "tile loads split evenly over the waves");
+  constexpr int kNBuf = NBUF;
   __shared__ Tile tiles[kNBuf];
   // paged caches: the split's page and value-alias entries, read into LDS once
   // (a table lookup per row would put a dependent load before every tile's loads)
@@ -388,14 +391,15 @@ __global__ void __launch_bounds__(WAVES * 64, 1) attn_prefill_mfma_kernel(
 
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, hipStream_t s, KTime tm) {
+                     int part_stride_rows, bool pair, hipStream_t s, KTime tm) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
-#define PF(DD, PG, WV)                                                                                      \
-  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta,     \
+  if (pair && waves != 4) return (int)hipErrorInvalidValue;
+#define PF(DD, PG, WV, NB)                                                                                  \
+  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta, \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFW(DD, PG) { if (waves == 8) PF(DD, PG, 8); else PF(DD, PG, 4); }
+#define PFW(DD, PG) { if (pair) PF(DD, PG, 4, 2); else if (waves == 8) PF(DD, PG, 8, 4); else PF(DD, PG, 4, 4); }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
   else { if (paged) PFW(64, true) else PFW(64, false) }

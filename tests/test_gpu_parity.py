@@ -368,6 +368,19 @@ def test_many_sequences_split_over_launches():
     run_pipeline(w, [0], 2, [0, 63, 64, 127, 128, 129])
 
 
+@pytest.mark.gpu
+def test_prefill_one_block_per_cu_path():
+    """64 sequences x 64 patch tokens at g = 4: 64 row blocks of 256 rows per kv head, 512
+    (row block, kv head) pairs, so the planner keeps one 8-wave block per CU (smaller calls
+    take two 4-wave blocks per CU)."""
+    from paper_2606_13097_amd import synth
+    shape = synth.Shape(1, 32, 8, 128, 1e6, "bf16")
+    n = 64
+    lengths = [60 + 5 * (i % 7) for i in range(n)]
+    w = synth.custom(shape, 17, lengths, [[i] for i in range(n)], n_fresh=64, n_decode=1)
+    run_pipeline(w, [0], 1, [0, 31, 63])
+
+
 def _tokens(w, tag, layer, item, rows):
     sh = w.shape
     q = tag.endswith("q")
