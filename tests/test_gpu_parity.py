@@ -381,6 +381,19 @@ def test_prefill_one_block_per_cu_path():
     run_pipeline(w, [0], 1, [0, 31, 63])
 
 
+@pytest.mark.gpu
+def test_paged_prefill_split_past_the_page_window():
+    """64 sequences share one 8,500-token segment (paged), 16 patch tokens each at g = 16: one
+    256-row block per sequence, 512 (row block, kv head) pairs, so one block per CU and one
+    unsplit key range of 533 pages, more than the 520 page entries a block keeps in LDS; the
+    blocks then read page-table entries per row."""
+    from paper_2606_13097_amd import synth
+    shape = synth.Shape(1, 128, 8, 64, 1e4, "bf16")
+    n = 64
+    w = synth.custom(shape, 23, [8500], [[0]] * n, n_fresh=16, n_decode=1, page_size=16)
+    run_pipeline(w, [0], 1, [0, 63])
+
+
 def _tokens(w, tag, layer, item, rows):
     sh = w.shape
     q = tag.endswith("q")
