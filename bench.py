@@ -78,6 +78,34 @@ def copy_probe(gib: float) -> None:
     log(f"copy probe: {n * 2} bytes read, {n * 2} bytes written")
 
 
+def copy_ceiling(total_bytes, graft_gbs, reps=10):
+    """A plain device-to-device copy (torch copy_) that reads and writes as many bytes as one
+    graft launch, timed on the same GPU: the practical ceiling for a pure stream."""
+    import torch
+    n = total_bytes // 4                     # bf16 elements per buffer: half the bytes each way
+    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        b.copy_(a)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = sorted(times)[len(times) // 2]
+    moved = 4 * n                            # read + write
+    del a, b
+    torch.cuda.empty_cache()
+    gbs = moved / (ms / 1e3) / 1e9
+    return {"kind": "device-to-device copy (torch copy_) of the graft launch's byte count, median of "
+                    f"{reps}", "bytes": moved, "us": round(ms * 1e3, 2), "gbs": round(gbs, 2),
+            "graft_over_copy": round(graft_gbs / gbs, 3)}
+
+
 def graft_bytes(tw, kvb, n_layers, alias_v):
     """Algorithmic graft bytes of one task: every grafted K and V row read once and
     written once; with value pages mapped onto the library, the values of pages a
@@ -468,6 +496,7 @@ def main():
         "note": "one task's grafted segments (all layers, K and V) to pinned host slabs and back, "
                 "including the call overhead; the paper's RTX 4090 figures per synthesis are 20.33 ms "
                 "(GPU to host) and 23.42 ms (host to GPU)"}
+    res["copy_ceiling"] = copy_ceiling(int(round(g_bytes / K)), graft_gbs)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(w, task_ws)
