@@ -1,8 +1,8 @@
 """Causal grouped-query attention over the grafted cache (oracle).
 
-Patching reuses the KV states of the prefix and computes only the new span
-(Sec. 4.2, Eq. 6; App. B.1, cache-patching), and every decode step attends to
-the whole cache built so far.  Reading of what the paper leaves open (the
+Only the new span's tokens are computed; they attend over the cached states
+before them (Sec. 4.2, Eq. 6; App. B.1, cache-patching), and every decode step
+attends to the whole cache built so far.  Reading of what the paper leaves open (the
 model is a Qwen2.5-Coder checkpoint run through HuggingFace Transformers,
 Sec. 5.1 and App. B.1): standard scaled-dot-product softmax attention, scale
 ``1 / sqrt(D)``, no soft-capping, bias or window; grouped-query heads with

@@ -228,10 +228,10 @@ class Layout:
     def truncate(self, seq: int, pos: int) -> None:
         """Keep only the prefix [0, pos) of a sequence, in every layer.
 
-        Cache-patching reuses the KV states of the preserved prefix and
-        regenerates the span after it (Sec. 4.2, Eq. 6; the patch step of
-        Alg. 1): the positions from the error span on are forgotten, and the
-        pages that hold no kept position return to the pool.
+        For cache-patching the cached states before the faulty span stay and
+        only what follows is generated again (Sec. 4.2, Eq. 6; the patch step
+        of Alg. 1): the positions from the error span on are forgotten, and
+        the pages that hold no kept position return to the pool.
         """
         if not (0 <= seq < self.n_seqs):
             raise FcgError(ERANGE, f"seq {seq}")

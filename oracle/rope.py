@@ -9,9 +9,9 @@ position ``p``, with ``w_i = theta ** (-2 i / D)``, ``i = 0 .. D/2 - 1``:
     y_i       = x_i       * cos(p w_i) - x_{i+D/2} * sin(p w_i)
     y_{i+D/2} = x_{i+D/2} * cos(p w_i) + x_i       * sin(p w_i)
 
-A cached function module is reused "without being tied to fixed prefix
-positions" (Sec. 4.1, two-tier code cache; the EPIC baseline of App. A.5
-likewise "transforms and aligns" cached key-value states).  A key stored
+A cached function module is reused wherever the new program places it (Sec.
+4.1, two-tier code cache; the EPIC baseline of App. A.5 likewise re-aligns
+cached key-value states to their new positions).  A key stored
 encoded at source position ``p_src`` and grafted at target position ``p_dst``
 is therefore turned by the delta ``p_dst - p_src``: since the rotations
 compose, ``R(delta) R(p_src) k = R(p_dst) k``.  Values carry no position and
