@@ -908,6 +908,10 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
       a.span = (int32_t)span;
       const size_t b1 = std::min(pf_rb.size(), b0 + (size_t)kPfMaxRb);
       a.n_rb = (int32_t)(b1 - b0);
+      // blocks of a split grouped on one XCD (shared L2) once four or more row
+      // blocks read its key tiles; with two, the pair ran in lockstep on
+      // neighbouring CUs and the call was 8% slower
+      a.xcd_group = a.n_rb >= 4;
       for (size_t b = b0; b < b1; ++b) {
         a.rb[b - b0] = pf_rb[b];
         a.n_split = std::max(a.n_split, pf_nsplit[b]);

@@ -49,6 +49,7 @@ __device__ __forceinline__ floatx4 mfma16x16x32(const uint4& a, const uint4& b, 
 }
 
 constexpr int kBN = 64;    // keys per tile
+constexpr int kXcds = 8;   // accelerator dies (XCDs) of the MI355X, each with its own L2
 
 template <int D>
 struct PrefillTile {
@@ -116,10 +117,29 @@ __global__ void __launch_bounds__(WAVES * 64, NBUF == 2 ? 2 : 1) attn_prefill_mf
   constexpr int NPG = PAGED ? kPageWindow : 1;
   __shared__ int32_t s_pg[NPG], s_al[NPG];
 
-  const PrefillRb rb = args.rb[blockIdx.x];
-  const int split = blockIdx.y;
-  const int hk = blockIdx.z;
+  // Block order.  Plain: grid (row block, split, kv head).  XCD-grouped
+  // (args.xcd_group): workgroups are dealt to the eight XCDs in turn by
+  // linear id (x fastest), so the row blocks that read the same key tiles
+  // (one group = one split of one kv head) get ids 8 apart and run on one XCD,
+  // whose L2 then serves the tiles after the first read: blockIdx.x = 8 r + x
+  // (row block r), blockIdx.y = q, group 8 q + x, numbered kv head fastest so
+  // that every XCD gets all the splits of its heads (late splits, which the
+  // causal mask leaves to fewer row blocks, spread over the XCDs).  Ids past
+  // the last group exit.
   const int Hkv = cv.n_kv_heads;
+  int rbi, split, hk;
+  if (args.xcd_group) {
+    const int xcd = blockIdx.x % kXcds;
+    rbi = blockIdx.x / kXcds;
+    const int grp = blockIdx.y * kXcds + xcd;
+    split = grp / Hkv;
+    hk = grp % Hkv;
+  } else {
+    rbi = blockIdx.x;
+    split = blockIdx.y;
+    hk = blockIdx.z;
+  }
+  const PrefillRb rb = args.rb[rbi];
   const int k0 = split * args.span;
   const int kend = min(rb.pmax + 1, k0 + args.span);
   const int part = rb.part0 < 0 ? -1 : rb.part0 + split;
@@ -132,7 +152,7 @@ __global__ void __launch_bounds__(WAVES * 64, NBUF == 2 ? 2 : 1) attn_prefill_mf
                "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(Hkv),
                "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
   if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
-  if (k0 >= kend) return;  // padding split of a shorter row block
+  if (split >= args.n_split || k0 >= kend) return;  // past the last group; padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
   const int lpa = k0 >> 4;
@@ -393,7 +413,9 @@ int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void*
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
                      int part_stride_rows, bool pair, hipStream_t s, KTime tm) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
-  dim3 grid(args.n_rb, args.n_split, cv.n_kv_heads);
+  const int groups = args.n_split * cv.n_kv_heads;  // (split, kv head) pairs
+  const dim3 grid = args.xcd_group ? dim3(kXcds * args.n_rb, (groups + kXcds - 1) / kXcds)
+                                   : dim3(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
   if (pair && waves != 4) return (int)hipErrorInvalidValue;
 #define PF(DD, PG, WV, NB)                                                                                  \

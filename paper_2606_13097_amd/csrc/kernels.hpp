@@ -155,7 +155,8 @@ struct PrefillRb {
   int32_t part0;       // first partial slot, -1 when the block has a single split
 };
 struct PrefillArgs {
-  int32_t n_rb, n_split, span, pad;
+  int32_t n_rb, n_split, span;
+  int32_t xcd_group;  // 1: row blocks of one (split, kv head) on one XCD (see the kernel)
   PrefillRb rb[kPfMaxRb];
 };
 
