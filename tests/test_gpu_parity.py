@@ -531,21 +531,22 @@ def _random_case(i):
              synth.Shape(1, 16, 1, 64, 1e4, "bf16"), synth.Shape(1, 32, 8, 128, 1e6, "bf16")][i % 4]
     n_seg = int(rng.integers(1, 7))
     lengths = [int(x) for x in rng.integers(1, 300, size=n_seg)]
-    n_seqs = int(rng.integers(1, 6))
+    n_seqs = int(rng.integers(1, 9))
     segs = [list(rng.choice(n_seg, size=int(rng.integers(1, min(n_seg, 3) + 1)), replace=False))
             for _ in range(n_seqs)]
     page = int(rng.choice([0, 16]))
     alias = bool(page and rng.integers(0, 2))
-    n_fresh, n_dec = int(rng.integers(1, 40)), int(rng.integers(1, 4))
+    n_fresh, n_dec = int(rng.integers(1, 100)), int(rng.integers(1, 4))
     w = synth.custom(shape, 2000 + i, lengths, segs, n_fresh=n_fresh, n_decode=n_dec, page_size=page)
     return w, n_dec, alias
 
 
 @pytest.mark.gpu
-@pytest.mark.parametrize("i", range(12))
+@pytest.mark.parametrize("i", range(24))
 def test_random_small_plans(i):
-    """Seeded random plans: 1-5 sequences grafting 1-3 of up to 6 segments of 1-299 tokens,
-    1-39 fresh tokens, 1-3 decode steps, over four head layouts, contiguous or paged caches,
-    values copied or read from the library; every sequence checked against the oracle."""
+    """Seeded random plans: 1-8 sequences grafting 1-3 of up to 6 segments of 1-299 tokens,
+    1-99 fresh tokens (one to a dozen MFMA row blocks per sequence, so both prefill block
+    orders), 1-3 decode steps, over four head layouts, contiguous or paged caches, values
+    copied or read from the library; every sequence checked against the oracle."""
     w, n_dec, alias = _random_case(i)
     run_pipeline(w, [0], n_dec, list(range(w.n_seqs)), alias=alias)
