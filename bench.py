@@ -47,6 +47,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe-gib", type=float, default=0.0,
                     help="only run a plain device copy of this size (HBM counter calibration)")
+    ap.add_argument("--gemm-probe", type=int, default=0,
+                    help="only run one bf16 GEMM n x n x n (matrix-op counter calibration)")
     return ap.parse_args()
 
 
@@ -54,8 +56,8 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def measured_traffic(name):
-    """HBM bytes per launch from a committed counter summary, if the kernel source is unchanged."""
+def measured_counter(name, field):
+    """A per-launch figure from a committed counter summary, if the kernel source is unchanged."""
     path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
@@ -64,7 +66,50 @@ def measured_traffic(name):
         d = json.load(f)
     if d.get("source_sha256") != source_sha256(d["source"]):
         return None
-    return int(round(d["traffic_bytes_per_launch"]))
+    return int(round(d[field]))
+
+
+def measured_traffic(name):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated by a plain copy)."""
+    return measured_counter(name, "traffic_bytes_per_launch")
+
+
+def gemm_probe(n: int) -> None:
+    import torch
+    a = torch.ones((n, n), dtype=torch.bfloat16, device="cuda")
+    b = torch.ones((n, n), dtype=torch.bfloat16, device="cuda")
+    torch.cuda.synchronize()
+    c = a @ b
+    torch.cuda.synchronize()
+    log(f"gemm probe: {n}^3 bf16, {2 * n ** 3} FLOP, c[0, 0] = {float(c[0, 0])}")
+
+
+def mfma_ceiling(attn_tflops, n=8192, reps=10):
+    """A bf16 GEMM (torch matmul, the vendor library's kernels) timed on the same GPU: the
+    practical matrix-core ceiling beside the published dense peak."""
+    import torch
+    g = torch.Generator(device="cuda").manual_seed(0)
+    a = torch.randn((n, n), dtype=torch.bfloat16, device="cuda", generator=g)
+    b = torch.randn((n, n), dtype=torch.bfloat16, device="cuda", generator=g)
+    for _ in range(2):
+        c = a @ b
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        c = a @ b
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = sorted(times)[len(times) // 2]
+    del a, b, c
+    torch.cuda.empty_cache()
+    tflops = 2.0 * n ** 3 / (ms / 1e3) / 1e12
+    return {"kind": f"bf16 GEMM {n} x {n} x {n} (torch matmul), median of {reps}", "us": round(ms * 1e3, 1),
+            "tflops": round(tflops, 1), "frac_of_peak": round(tflops / BF16_PEAK_TFLOPS, 4),
+            "patch_attn_over_gemm": round(attn_tflops / tflops, 4)}
 
 
 def copy_probe(gib: float) -> None:
@@ -232,6 +277,9 @@ def main():
 
     if args.copy_probe_gib > 0:
         copy_probe(args.copy_probe_gib)
+        return
+    if args.gemm_probe > 0:
+        gemm_probe(args.gemm_probe)
         return
     torch.cuda.set_device(0)
     nd = args.decode_steps
@@ -461,6 +509,7 @@ def main():
             {"bound": "mfma", "kernel": "fcg attn_prefill_mfma_kernel", "achieved": round(attn_tflops, 3),
              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)}) | {
             "traffic": measured_traffic("prefill_7b_traffic.json"),
+            "counter_flops_per_launch": measured_counter("prefill_7b_mfma.json", "counter_flops_per_launch"),
             "algorithmic_flops_per_launch": int(round(p_flops / (K * sh.n_layers))),
             "algorithmic_bytes_per_launch": int(round(p_bytes / (K * sh.n_layers))),
             "intensity_flop_per_byte": round(p_intensity, 1),
@@ -497,6 +546,10 @@ def main():
                 "including the call overhead; the paper's RTX 4090 figures per synthesis are 20.33 ms "
                 "(GPU to host) and 23.42 ms (host to GPU)"}
     res["copy_ceiling"] = copy_ceiling(int(round(g_bytes / K)), graft_gbs)
+    res["mfma_ceiling"] = mfma_ceiling(attn_tflops)
+    cf = res["roofline_patch_attn"]["counter_flops_per_launch"]
+    if cf:
+        res["roofline_patch_attn"]["counter_tflops"] = round(cf / (a_kms / 1e3 / (K * sh.n_layers)) / 1e12, 3)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
         res["cpu_baseline"] = cpu_baseline(w, task_ws)

@@ -4,11 +4,15 @@
     python -m paper_2606_13097_amd.profiling traffic --kernel graft_kernel --source csrc/k_graft.hip \
         --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv --copy-bytes 1073741824 \
         --skip 1 --command C
+    python -m paper_2606_13097_amd.profiling mfma --kernel attn_prefill_mfma_kernel \
+        --source csrc/k_attn_mfma.hip --ops OPS.csv --gemm-ops GEMM.csv --gemm-flops 1.37e11 --command C
 
 ``traffic`` averages the kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) over its
 dispatches after the first ``--skip`` ones, and calibrates each counter by what it reads
-for a plain device copy of ``--copy-bytes`` bytes.  The JSON records the SHA-256 of the
-kernel's source files: ``bench.py`` reports the traffic only while they are unchanged.
+for a plain device copy of ``--copy-bytes`` bytes.  ``mfma`` does the same for the bf16
+matrix-op counter SQ_INSTS_VALU_MFMA_MOPS_BF16, calibrated by a bf16 GEMM of known FLOPs
+(``--gemm-flops``; its largest dispatch).  Each JSON records the SHA-256 of the kernel's
+source files: ``bench.py`` reports the figures only while they are unchanged.
 """
 from __future__ import annotations
 
@@ -78,6 +82,30 @@ def traffic(args) -> dict:
             "command": args.command}
 
 
+def _sum_per_dispatch(path: str, kernel: str, counter: str):
+    """Counter values summed per dispatch (a raw counter may come in several rows)."""
+    acc = {}
+    for r in csv.DictReader(open(path)):
+        if kernel in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            d = int(r["Dispatch_Id"])
+            acc[d] = acc.get(d, 0.0) + float(r["Counter_Value"])
+    return [acc[d] for d in sorted(acc)]
+
+
+MOPS = "SQ_INSTS_VALU_MFMA_MOPS_BF16"
+
+
+def mfma(args) -> dict:
+    end = args.skip + args.take if args.take else None
+    m = _sum_per_dispatch(args.ops, args.kernel, MOPS)[args.skip:end]
+    g = max(_sum_per_dispatch(args.gemm_ops, "", MOPS))
+    per_op = args.gemm_flops / g
+    return {"kernel": args.kernel, "source": args.source, "source_sha256": source_sha256(args.source),
+            "counter": MOPS, "dispatches": len(m), "ops_avg": sum(m) / len(m), "flops_per_op": per_op,
+            "gemm_flops": args.gemm_flops, "gemm_ops": g,
+            "counter_flops_per_launch": sum(m) / len(m) * per_op, "command": args.command}
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -92,11 +120,17 @@ def main(argv=None):
     t.add_argument("--copy-bytes", type=float, default=float(1 << 30))
     t.add_argument("--skip", type=int, default=0, help="dispatches to leave out first (warm-up)")
     t.add_argument("--take", type=int, default=0, help="dispatches to average after those (0: all)")
+    m = sub.add_parser("mfma")
+    for k in ("kernel", "source", "ops", "gemm_ops", "command"):
+        m.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
+    m.add_argument("--gemm-flops", type=float, required=True)
+    m.add_argument("--skip", type=int, default=0)
+    m.add_argument("--take", type=int, default=0)
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         sys.stdout.write(stats_markdown(a.csv, a.title, a.command))
     else:
-        json.dump(traffic(a), sys.stdout, indent=1)
+        json.dump(traffic(a) if a.cmd == "traffic" else mfma(a), sys.stdout, indent=1)
         sys.stdout.write("\n")
 
 
