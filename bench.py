@@ -84,6 +84,36 @@ def gemm_probe(n: int) -> None:
     log(f"gemm probe: {n}^3 bf16, {2 * n ** 3} FLOP, c[0, 0] = {float(c[0, 0])}")
 
 
+def mfma_rate(shape, blocks=512, iters=10000, reps=5):
+    """The matrix cores' sustained bf16 rate: register-only MFMA chains on every SIMD
+    (measure/libfcg_measure.so; shape 0: 16x16x32, 1: 32x32x16), FLOP count / kernel
+    time, median of ``reps``."""
+    import ctypes as C
+    import torch
+    lib = C.CDLL(os.path.join(ROOT, "paper_2606_13097_amd", "measure", "libfcg_measure.so"))
+    lib.fcg_measure_mfma_rate.argtypes = [C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_int]
+    lib.fcg_measure_mfma_rate.restype = C.c_int
+    out = torch.empty(blocks * 256, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    if lib.fcg_measure_mfma_rate(blocks, 100, C.c_void_p(out.data_ptr()), C.c_void_p(stream), shape):
+        raise RuntimeError("fcg_measure_mfma_rate failed")
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        lib.fcg_measure_mfma_rate(blocks, iters, C.c_void_p(out.data_ptr()), C.c_void_p(stream), shape)
+        e1.record()
+        e1.synchronize()
+        times.append(e0.elapsed_time(e1))
+    ms = sorted(times)[len(times) // 2]
+    tflops = blocks * 4 * iters * 131072 / (ms / 1e3) / 1e12
+    inst = "v_mfma_f32_16x16x32_bf16" if shape == 0 else "v_mfma_f32_32x32x16_bf16"
+    return {"kind": f"register-only {inst} chains, {blocks} blocks of 4 waves, median of {reps}",
+            "us": round(ms * 1e3, 1), "tflops": round(tflops, 1), "frac_of_peak": round(tflops / BF16_PEAK_TFLOPS, 4)}
+
+
 def mfma_ceiling(attn_tflops, n=8192, reps=10):
     """A bf16 GEMM (torch matmul, the vendor library's kernels) timed on the same GPU: the
     practical matrix-core ceiling beside the published dense peak."""
@@ -547,6 +577,8 @@ def main():
                 "(GPU to host) and 23.42 ms (host to GPU)"}
     res["copy_ceiling"] = copy_ceiling(int(round(g_bytes / K)), graft_gbs)
     res["mfma_ceiling"] = mfma_ceiling(attn_tflops)
+    res["mfma_ceiling"]["issue_rate"] = mfma_rate(0)
+    res["mfma_ceiling"]["issue_rate_32x32x16"] = mfma_rate(1)
     cf = res["roofline_patch_attn"]["counter_flops_per_launch"]
     if cf:
         res["roofline_patch_attn"]["counter_tflops"] = round(cf / (a_kms / 1e3 / (K * sh.n_layers)) / 1e12, 3)

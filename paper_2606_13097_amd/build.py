@@ -3,8 +3,10 @@
     python -m paper_2606_13097_amd.build        # or __graft_entry__.build()
 
 Produces ``paper_2606_13097_amd/libfcg.so`` (the grafting hot path, C ABI in
-``include/fcg.h``) and ``paper_2606_13097_amd/synth/libfcg_synth.so`` (the
-device twin of the seeded input generator).  Every call recompiles.
+``include/fcg.h``), ``paper_2606_13097_amd/synth/libfcg_synth.so`` (the
+device twin of the seeded input generator) and
+``paper_2606_13097_amd/measure/libfcg_measure.so`` (a matrix-core rate probe
+for the bench).  Every call recompiles.
 """
 from __future__ import annotations
 
@@ -40,6 +42,7 @@ LIBS = {
          "k_decode.hip", "k_decode_mfma.hip")
     ],
     os.path.join(PKG, "synth", "libfcg_synth.so"): [os.path.join(PKG, "synth", "synth.hip")],
+    os.path.join(PKG, "measure", "libfcg_measure.so"): [os.path.join(PKG, "measure", "peak.hip")],
 }
 
 
