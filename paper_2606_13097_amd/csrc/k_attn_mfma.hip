@@ -3,10 +3,11 @@
 // accumulation, fp32 online softmax in base 2.
 //
 // Block: 4 or 8 waves, 32 query rows each, of one kv head (the g query heads
-// of consecutive tokens of one sequence; 8 waves hold all 256 rows of a
-// 64-token patch at g = 4, so every K/V tile is read once per head), and one
-// split [k0, k1) of the key positions.  Wave w owns rows 32w .. 32w + 31 as
-// two 16-row tiles.
+// of consecutive tokens of one sequence), and one split [k0, k1) of the key
+// positions.  Wave w owns rows 32w .. 32w + 31 as two 16-row tiles.  The host
+// picks the shape per call: 4-wave blocks sized to run two per CU (the two
+// blocks' softmax and matrix phases overlap), or, when 256-row blocks alone
+// fill the chip twice, 8-wave blocks one per CU.
 //
 // Key tiles of 64 keys go from memory straight into LDS (global_load_lds:
 // each instruction fills 1 KB, 16 bytes per lane), into a ring of four
