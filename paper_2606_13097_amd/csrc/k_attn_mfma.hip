@@ -96,11 +96,14 @@ __device__ __forceinline__ uint2 ld_tr8(const bf16_t* p) {
 }
 
 // grid (row block, key split, kv head).  NBUF tiles in the LDS ring: 4 (three
-// in flight while one is attended) for one block per CU, 2 (132 KB against
-// 68 KB of LDS at D 128) for two 4-wave blocks per CU, whose phases then
-// overlap (one block's softmax beside the other's matrix work).
+// in flight while one is attended) for 8-wave blocks and 4-wave blocks of the
+// plain one-per-CU plan, 2 (132 KB against 68 KB of LDS at D 128) for 4-wave
+// blocks planned two per CU, whose phases then overlap (one block's softmax
+// beside the other's matrix work).  4-wave blocks aim at 256 registers per
+// lane (two waves per SIMD); the four-tile ring at D 128 still needs more,
+// and the compiler keeps its accumulators in AGPRs.
 template <int D, bool PAGED, int WAVES, int NBUF>
-__global__ void __launch_bounds__(WAVES * 64, NBUF == 2 ? 2 : 1) attn_prefill_mfma_kernel(
+__global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
     float* __restrict__ part_ml, int part_stride_rows) {
@@ -412,17 +415,17 @@ __global__ void __launch_bounds__(WAVES * 64, NBUF == 2 ? 2 : 1) attn_prefill_mf
 
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, bool pair, hipStream_t s, KTime tm) {
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   const int groups = args.n_split * cv.n_kv_heads;  // (split, kv head) pairs
   const dim3 grid = args.xcd_group ? dim3(kXcds * args.n_rb, (groups + kXcds - 1) / kXcds)
                                    : dim3(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
-  if (pair && waves != 4) return (int)hipErrorInvalidValue;
+  if ((nbuf != 2 && nbuf != 4) || (nbuf == 2 && waves != 4)) return (int)hipErrorInvalidValue;
 #define PF(DD, PG, WV, NB)                                                                                  \
   hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta, \
                      (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFW(DD, PG) { if (pair) PF(DD, PG, 4, 2); else if (waves == 8) PF(DD, PG, 8, 4); else PF(DD, PG, 4, 4); }
+#define PFW(DD, PG) { if (nbuf == 2) PF(DD, PG, 4, 2); else if (waves == 8) PF(DD, PG, 8, 4); else PF(DD, PG, 4, 4); }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
   else { if (paged) PFW(64, true) else PFW(64, false) }

@@ -161,10 +161,11 @@ struct PrefillArgs {
 };
 
 // bf16 MFMA attention of query-workspace rows over the cache.  Blocks of
-// part_stride_rows / 32 waves; pair: 4-wave blocks sized for two per CU.
+// part_stride_rows / 32 waves; nbuf: tiles of the LDS ring, 2 for 4-wave
+// blocks sized to run two per CU, else 4.
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, bool pair, hipStream_t s, KTime tm = {});
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm = {});
 
 // VALU attention, one token (g query rows) per item; any dtype.
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
