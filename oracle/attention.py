@@ -56,11 +56,3 @@ def attend(q, positions, K, V, written) -> np.ndarray:
     return np.stack([attend_row(q[t], int(p), K, V, written) for t, p in enumerate(positions)]) \
         if len(positions) else np.zeros((0,) + q.shape[1:])
 
-
-def attend_head(q_row, p: int, K, V, hq: int, group: int) -> np.ndarray:
-    """A single (token, query head) output; for sampling large caches."""
-    h = hq // group
-    keys = K[:p + 1, h, :]
-    s = keys @ np.asarray(q_row, dtype=np.float64) / np.sqrt(K.shape[2])
-    e = np.exp(s - s.max())
-    return (e / e.sum()) @ V[:p + 1, h, :]

@@ -2,6 +2,7 @@
 from __future__ import annotations
 
 import ctypes
+import os
 import sys
 
 import numpy as np
@@ -111,27 +112,62 @@ def scale_storage(x: np.ndarray, mult: float, dtype: str) -> np.ndarray:
     return numerics.encode(numerics.decode(x, dtype) * mult, dtype)
 
 
-def check_attn(got_storage: np.ndarray, ref: np.ndarray, dtype: str, what: str) -> None:
-    """fp32: normwise 1e-5 per head; bf16: max-abs 2e-2 * max(1, max|ref|) and relative Frobenius 1e-2.
+# bf16 keeps 8 significant bits: one round-to-nearest step changes a value x by
+# at most U_BF16 * |x|
+U_BF16 = 2.0 ** -8
+# Roundings on the bf16 attention path that scale with the output element: its own
+# storage rounding, the bf16 probabilities of the PV product (for a dominant key
+# the output is that key's value times its rounded weight), and the bf16 split
+# partials that the merge of a split key range reads.
+C_ATTN = 3 * U_BF16
+ABS_ATTN = 2e-2          # max-abs bar on bf16 attention outputs
+FRO_ATTN = 1e-2          # relative Frobenius bar (2e-2 max-abs is vacuous for near-uniform attention)
 
-    The 2e-2 max-abs bar is for unit-scale outputs: bf16 storage of an output of size |o|
-    alone carries up to 2^-9 |o| of rounding, so workloads whose values reach |o| > 1 (the
-    x8 outlier channels) scale the bar with the largest reference magnitude.
+# Observed errors of every check of the session, printed in pytest's terminal
+# summary (tests/conftest.py) so that the margins appear in the log of passing runs.
+STATS: list = []
+
+
+def _record(kind: str, what: str, **fields) -> None:
+    test = os.environ.get("PYTEST_CURRENT_TEST", "").split(" ")[0]
+    STATS.append(dict(kind=kind, what=what, test=test, **fields))
+
+
+def check_attn(got_storage: np.ndarray, ref: np.ndarray, dtype: str, what: str) -> dict:
+    """fp32: normwise 1e-5 per head.  bf16: per element |got - ref| <= 2e-2 + C_ATTN |ref|,
+    and relative Frobenius 1e-2 over the tensor.
+
+    The absolute 2e-2 is the bar on bf16 attention outputs; the per-element term
+    covers the roundings that scale with the element itself (C_ATTN), which matter
+    once outputs reach magnitudes of several units (x8 outlier channels, peaked
+    attention onto one large value).
     """
     got = numerics.decode(got_storage, dtype)
     assert got.shape == ref.shape, (got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{what}: non-finite output"
     if dtype == "f32":
+        worst = 0.0
         for h in range(ref.shape[-2]):
             den = np.abs(ref[..., h, :]).max()
             err = np.abs(got[..., h, :] - ref[..., h, :]).max()
+            worst = max(worst, err / den if den > 0 else err)
             assert err <= 1e-5 * den, f"{what}: head {h} normwise error {err / den:.3e} > 1e-5"
-    else:
-        err = np.abs(got - ref).max()
-        fro = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
-        lim = 2e-2 * max(1.0, float(np.abs(ref).max()))
-        assert err <= lim, f"{what}: max-abs error {err:.3e} > {lim:.3e}"
-        assert fro <= 1e-2, f"{what}: relative Frobenius error {fro:.3e} > 1e-2"
+        _record("attn-f32", what, normwise=worst)
+        return {"normwise": worst}
+    diff = np.abs(got - ref)
+    bar = ABS_ATTN + C_ATTN * np.abs(ref)
+    use = float((diff / bar).max()) if diff.size else 0.0
+    err = float(diff.max()) if diff.size else 0.0
+    fro = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
+    # the smallest per-element coefficient this check needed beyond the absolute bar
+    need_c = float(np.max((diff - ABS_ATTN) / np.maximum(np.abs(ref), 1e-30), initial=0.0))
+    st = {"max_abs": err, "fro": fro, "bar_use": use, "need_c": max(need_c, 0.0),
+          "max_ref": float(np.abs(ref).max()) if ref.size else 0.0}
+    _record("attn-bf16", what, **st)
+    assert use <= 1.0, (f"{what}: |got - ref| exceeds 2e-2 + {C_ATTN:.4g} |ref| (worst element at "
+                        f"{use:.3f} of its bar, max-abs {err:.3e})")
+    assert fro <= FRO_ATTN, f"{what}: relative Frobenius error {fro:.3e} > {FRO_ATTN}"
+    return st
 
 
 def check_keys(got_storage: np.ndarray, ref_rounded: np.ndarray, dtype: str, what: str) -> None:
@@ -148,6 +184,7 @@ def check_keys(got_storage: np.ndarray, ref_rounded: np.ndarray, dtype: str, wha
     if dtype == "f32":
         den = np.abs(ref_rounded).max()
         err = np.abs(got - ref_rounded).max()
+        _record("keys-f32", what, normwise=float(err / den) if den > 0 else float(err))
         assert err <= 1e-5 * den, f"{what}: normwise error {err / den:.3e}"
     else:
         half = ref_rounded.shape[-1] // 2
@@ -155,6 +192,7 @@ def check_keys(got_storage: np.ndarray, ref_rounded: np.ndarray, dtype: str, wha
         pair = np.concatenate([pair, pair], axis=-1)
         tol = numerics.ulp(ref_rounded, dtype) + 2.0 ** -20 * pair
         bad = np.abs(got - ref_rounded) > tol
-        assert not bad.any(), f"{what}: {int(bad.sum())} keys outside one ulp + 2^-20 |pair|"
         n_off = int((got != ref_rounded).sum())
+        _record("keys-bf16", what, off_rounding=n_off, n=int(got.size), outside_bar=int(bad.sum()))
+        assert not bad.any(), f"{what}: {int(bad.sum())} keys outside one ulp + 2^-20 |pair|"
         assert n_off <= 0.01 * got.size, f"{what}: {n_off} of {got.size} keys differ from the oracle's rounding"
