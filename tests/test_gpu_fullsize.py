@@ -63,3 +63,47 @@ def test_7b_full_size_sampled(task):
         say("[gpu]   parity ok")
     finally:
         s.close()
+
+
+# The other full-size workloads: the plans are not trimmed (every segment, every
+# patch token, the library at its full size in HBM); prefill and two decode steps
+# run on the first, a middle and the last layer, and the oracle checks sampled
+# sequences there (layout of every sequence bit for bit, grafted and final keys and
+# values, prefill and decode outputs).
+
+def _sampled_layers(n_layers):
+    return [0, n_layers // 2, n_layers - 1]
+
+
+@pytest.mark.timeout(900)
+def test_long16k_full_size_sampled():
+    """~16K-token context: 2048-token prefix + 20 segments of U[400,1200] with 0-32 fresh gap
+    tokens before each, 256 patch tokens prefilled in the same call."""
+    from test_gpu_parity import run_pipeline
+    from paper_2606_13097_amd import synth
+    w = synth.workload("long16k", seed=1, n_decode=2)
+    say(f"[gpu] full-size long16k: {w.grafted_tokens} grafted, {len(w.fresh_pos)} fresh tokens")
+    run_pipeline(w, _sampled_layers(w.shape.n_layers), 2, [0])
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("alias", [False, True])
+def test_batched_full_size_sampled(alias):
+    """32 tasks x 8 Zipf-drawn segments from the 512-segment library, 16-token pages, 32 patch
+    tokens per task; values copied or read from the library (FCG_ALIAS_V)."""
+    from test_gpu_parity import run_pipeline
+    from paper_2606_13097_amd import synth
+    w = synth.workload("batched", seed=1, n_decode=2)
+    say(f"[gpu] full-size batched alias={alias}: {w.grafted_tokens} grafted tokens over {w.n_seqs} tasks")
+    run_pipeline(w, _sampled_layers(w.shape.n_layers), 2, [0, 13, 31], alias=alias)
+
+
+@pytest.mark.timeout(1200)
+def test_34b_full_size_sampled():
+    """48 layers, 64/8 heads, 1024-segment library (~182 GB) with 1% outlier pairs x8; 4 tasks
+    of 24 segments and 512 patch tokens each."""
+    from test_gpu_parity import run_pipeline
+    from paper_2606_13097_amd import synth
+    w = synth.workload("34b", seed=1, n_decode=2)
+    say(f"[gpu] full-size 34b: {w.grafted_tokens} grafted tokens over {w.n_seqs} tasks")
+    run_pipeline(w, _sampled_layers(w.shape.n_layers), 2, [0, 3])
