@@ -223,6 +223,7 @@ struct fcg_cache {
   int64_t layer_stride = 0;
   int32_t* d_page_table = nullptr;
   double* d_inv_freq = nullptr;
+  float2* d_rope = nullptr;   // (cos, sin) per position and rotary pair [max_tokens][D/2]
   int device = 0;
   Ring ring;
   // workspaces, grown on demand
@@ -633,6 +634,18 @@ fcg_status fcg_cache_create(const fcg_model_desc* desc, int32_t n_seqs, int32_t 
       fcg_cache_destroy(c);
       return st;
     }
+    // rotary table of every position the cache can hold, computed once here
+    const int half = desc->head_dim / 2;
+    if (hipMalloc((void**)&c->d_rope, (size_t)max_tokens * half * sizeof(float2)) != hipSuccess) {
+      fcg_cache_destroy(c);
+      return fail(FCG_ENOMEM, "rotary table does not fit in device memory");
+    }
+    int rc = launch_rope_table(c->d_inv_freq, half, max_tokens, c->d_rope, nullptr);
+    if (rc == 0) rc = (int)hipStreamSynchronize(nullptr);
+    if (rc) {
+      fcg_cache_destroy(c);
+      return hip_fail((hipError_t)rc, "rotary table");
+    }
 
   }
   *out = c;
@@ -748,6 +761,7 @@ fcg_status fcg_cache_destroy(fcg_cache* c) {
     if (c->v) hipFree(c->v);
     if (c->d_page_table) hipFree(c->d_page_table);
     if (c->d_inv_freq) hipFree(c->d_inv_freq);
+    if (c->d_rope) hipFree(c->d_rope);
     if (c->qws) hipFree(c->qws);
     if (c->part) hipFree(c->part);
     if (c->dpart) hipFree(c->dpart);
@@ -955,7 +969,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   // launches bracket their own, the last kernel closes the call's
   const hipEvent_t e_call0 = timing_event(c), e_attn0 = timing_event(c), e_attn1 = timing_event(c);
   const hipEvent_t e_call1 = comb.empty() ? e_attn1 : timing_event(c);
-  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_inv_freq, d.n_q_heads, c->qws, s,
+  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_rope, d.n_q_heads, c->qws, s,
                               KTime{e_call0, nullptr});
   if (rc) return hip_fail((hipError_t)rc, "append launch");
   float* part_o = c->part;
@@ -992,13 +1006,15 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   return c->ring.retire(off, blob.bytes.size(), s);
 }
 
-// One decode launch per group of up to kMaxDecodeSeqs sequences; the launch
-// merges the splits of each sequence itself and takes its plan by value, so a
-// decode step uploads nothing (new pages aside).
-fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
-                      const void* q, const void* k, const void* v, void* out,
-                      const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
-  const fcg_model_desc& d = c->desc;
+// Split plan of one decode call: split length in keys and the largest number
+// of partial slots any launch group needs.
+struct DecodePlan {
+  int64_t split_keys = 0;
+  int max_slots = 0;
+  size_t part_o = 0, part_ml = 0;  // floats of the partial outputs and of the (max, sum) pairs
+};
+
+DecodePlan plan_decode(const fcg_model_desc& d, int32_t n, const std::vector<int32_t>& pos) {
   const int g = d.n_q_heads / d.n_kv_heads;
   int64_t total = 0;
   int32_t pmax = 0;
@@ -1022,29 +1038,32 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     sk += (sk + 31) / 32;  // about 3% longer
   }
   sk = (sk + 63) / 64 * 64;
+  DecodePlan p;
+  p.split_keys = sk;
   // partial slots: one per split of every multi-split sequence of a launch group
-  int max_slots = 0;
   for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {
     int slots = 0;
     for (int32_t i = i0; i < std::min<int32_t>(n, i0 + kMaxDecodeSeqs); ++i) slots += (int)((pos[i] + sk) / sk);
-    max_slots = std::max(max_slots, slots);
+    p.max_slots = std::max(p.max_slots, slots);
   }
-  const size_t po = (size_t)max_slots * d.n_kv_heads * g * d.head_dim, pml = (size_t)max_slots * d.n_kv_heads * g * 2;
-  if (fcg_status st = grow((void**)&c->dpart, &c->dpart_bytes, (po + pml) * sizeof(float), "decode partials"))
-    return st;
-  if (!new_pages.empty()) {
-    Blob blob;
-    std::vector<std::pair<int32_t, size_t>> rows;
-    stage_pages(c, new_pages, &blob, &rows);
-    char* dev;
-    size_t off;
-    if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
-    if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
-  }
+  p.part_o = (size_t)p.max_slots * d.n_kv_heads * g * d.head_dim;
+  p.part_ml = (size_t)p.max_slots * d.n_kv_heads * g * 2;
+  return p;
+}
+
+// One decode launch per group of up to kMaxDecodeSeqs sequences; the launch
+// merges the splits of each sequence itself and takes its plan by value
+// (pages the step maps included), so a decode step uploads nothing.
+// part_o / part_ml / count: the partial and counter buffers (the cache's own,
+// or the static scratch of the allocation-free entry point).
+fcg_status launch_decode_groups(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs,
+                                const std::vector<int32_t>& pos, const std::vector<int32_t>& new_page,
+                                const DecodePlan& plan, const void* q, const void* k, const void* v, void* out,
+                                float* part_o, float* part_ml, int32_t* count, bool timing, hipStream_t s) {
+  const fcg_model_desc& d = c->desc;
   const CacheView cv = c->view();
   const size_t es = esize(d.dtype);
-  float* part_o = c->dpart;
-  float* part_ml = c->dpart + po;
+  const int64_t sk = plan.split_keys;
   for (int32_t i0 = 0; i0 < n; i0 += kMaxDecodeSeqs) {
     DecodeArgs a{};
     a.n = std::min<int32_t>(kMaxDecodeSeqs, n - i0);
@@ -1053,28 +1072,56 @@ fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seq
     for (int32_t i = 0; i < a.n; ++i) {
       a.seq[i] = seqs[i0 + i];
       a.pos[i] = pos[i0 + i];
+      a.new_page[i] = new_page[i0 + i];
       const int32_t ns = (int32_t)((pos[i0 + i] + sk) / sk);
       a.split0[i + 1] = a.split0[i] + ns;
       a.max_split = std::max(a.max_split, ns);
     }
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
     // timing: one kernel, both intervals
-    const hipEvent_t e0 = timing_event(c), e1 = timing_event(c);
+    const hipEvent_t e0 = timing ? timing_event(c) : nullptr, e1 = timing ? timing_event(c) : nullptr;
     // bf16: matrix-core kernel; fp32: the vector-ALU kernel
     int rc = d.dtype == FCG_BF16
                  ? launch_decode_mfma(a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv,
-                                      layer, c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml,
-                                      c->d_count, s, KTime{e0, e1})
+                                      layer, c->d_rope, d.n_q_heads, (char*)out + qoff, part_o, part_ml, count, s,
+                                      KTime{e0, e1})
                  : launch_decode(d.dtype, a, (const char*)q + qoff, (const char*)k + koff, (const char*)v + koff, cv,
-                                 layer, c->d_inv_freq, d.n_q_heads, (char*)out + qoff, part_o, part_ml, c->d_count, s,
+                                 layer, c->d_rope, d.n_q_heads, (char*)out + qoff, part_o, part_ml, count, s,
                                  KTime{e0, e1});
     if (rc) return hip_fail((hipError_t)rc, "decode launch");
-    time_open(c, FCG_TIME_DECODE_ATTN, e0);
-    time_close(c, FCG_TIME_DECODE_ATTN, e1);
-    time_open(c, FCG_TIME_DECODE, e0);
-    time_close(c, FCG_TIME_DECODE, e1);
+    if (timing) {
+      time_open(c, FCG_TIME_DECODE_ATTN, e0);
+      time_close(c, FCG_TIME_DECODE_ATTN, e1);
+      time_open(c, FCG_TIME_DECODE, e0);
+      time_close(c, FCG_TIME_DECODE, e1);
+    }
   }
   return FCG_OK;
+}
+
+// The physical page each sequence's new token lands on when this step maps
+// its page (the planner's mapping, already committed), else -1.
+std::vector<int32_t> decode_new_pages(const fcg_cache* c, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
+                                      const std::vector<std::pair<int32_t, int32_t>>& new_pages) {
+  std::vector<int32_t> np(n, -1);
+  if (new_pages.empty()) return np;
+  for (int32_t i = 0; i < n; ++i)
+    for (auto& sl : new_pages)
+      if (sl.first == seqs[i] && sl.second == pos[i] / c->page_size) np[i] = c->plan.page_of(seqs[i], pos[i]);
+  return np;
+}
+
+fcg_status run_decode(fcg_cache* c, int32_t layer, int32_t n, const int32_t* seqs, const std::vector<int32_t>& pos,
+                      const void* q, const void* k, const void* v, void* out,
+                      const std::vector<std::pair<int32_t, int32_t>>& new_pages, hipStream_t s) {
+  const DecodePlan plan = plan_decode(c->desc, n, pos);
+  if (fcg_status st = grow((void**)&c->dpart, &c->dpart_bytes, (plan.part_o + plan.part_ml) * sizeof(float),
+                           "decode partials"))
+    return st;
+  c->plan.map_pages(new_pages);
+  const std::vector<int32_t> np = decode_new_pages(c, n, seqs, pos, new_pages);
+  return launch_decode_groups(c, layer, n, seqs, pos, np, plan, q, k, v, out, c->dpart, c->dpart + plan.part_o,
+                              c->d_count, c->timing, s);
 }
 
 }  // namespace

@@ -18,6 +18,27 @@
 
 namespace fcg {
 
+// Element offset of the new token's row (layer, seq, head, pos).  A page the
+// step maps comes by value (DecodeArgs::new_page): the device page table gets
+// its entry from this launch (enter_page), so no block reads it there.
+template <bool PAGED>
+__device__ __forceinline__ int64_t new_token_offset(const CacheView& c, int layer, int seq, int head, int pos,
+                                                    int new_page) {
+  if (PAGED && new_page >= 0)
+    return (int64_t)layer * c.layer_stride +
+           (((int64_t)new_page * c.n_kv_heads + head) * 16 + (pos & 15)) * c.head_dim;
+  return kv_offset<PAGED>(c, layer, seq, head, pos);
+}
+
+// The device page-table entries of a page a decode step maps: its physical
+// page, and "values not read from the library" (written by one lane of the
+// owning split's first kv-head block; later launches read them).
+__device__ __forceinline__ void enter_page(const CacheView& c, int seq, int pos, int new_page) {
+  int32_t* row = const_cast<int32_t*>(c.page_table) + (int64_t)seq * 2 * c.n_lp;
+  row[pos >> 4] = new_page;
+  row[c.n_lp + (pos >> 4)] = -1;
+}
+
 // partial slot row of (split slot, kv head, query head): [slot][Hkv][G]
 __device__ __forceinline__ int64_t part_row(int slot, int Hkv, int hk, int G, int j) {
   return ((int64_t)slot * Hkv + hk) * G + j;

@@ -1,6 +1,6 @@
 // Fresh-token encoding and append for gfx950 (patch prefill and decode steps,
-// Sec. 4.2, Eq. 6).  One block per token: the block computes the D/2 cos/sin
-// of its position once (LDS), then its lanes turn every rotary pair of the
+// Sec. 4.2, Eq. 6).  One block per token: the block reads the D/2 cos/sin of
+// its position from the cache's rotary table (LDS), then its lanes turn every rotary pair of the
 // token's query and key heads and store
 //   - the key (rounded to storage) and the value into the cache slot of the
 //     token's position in this layer,
@@ -16,7 +16,7 @@ template <typename T, int D>
 __global__ void __launch_bounds__(256) rope_append_kernel(const TokenMeta* __restrict__ meta,
                                                           const T* __restrict__ q, const T* __restrict__ k,
                                                           const T* __restrict__ v, CacheView cv, int layer,
-                                                          const double* __restrict__ inv_freq, int Hq,
+                                                          const float2* __restrict__ rope, int Hq,
                                                           int rows_ws, T* __restrict__ qws) {
   constexpr int VEC = Store<T>::VEC;
   constexpr int HALF = D / 2;
@@ -83,8 +83,11 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const TokenMeta* __res
       pb[p] = rot ? ld16(src + HALF) : pa[p];
     }
   }
-  const double w = inv_freq[t % HALF];
-  if (t < HALF) rope_cs((double)m.pos, w, &s_cos[t], &s_sin[t]);
+  const float2 cs = rope[(int64_t)m.pos * HALF + t % HALF];  // (cos, sin) of the token's position
+  if (t < HALF) {
+    s_cos[t] = cs.x;
+    s_sin[t] = cs.y;
+  }
   __syncthreads();
 #pragma unroll
   for (int p = 0; p < PRE; ++p) {
@@ -100,15 +103,37 @@ __global__ void __launch_bounds__(256) rope_append_kernel(const TokenMeta* __res
 }
 
 int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, const void* k, const void* v,
-                       const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws, hipStream_t s, KTime tm) {
+                       const CacheView& cv, int layer, const float2* rope, int Hq, void* qws, hipStream_t s, KTime tm) {
   if (n == 0) return 0;
   const int rows_ws = n * (Hq / cv.n_kv_heads);
 #define RA(T, DD)                                                                                          \
   hipExtLaunchKernelGGL((rope_append_kernel<T, DD>), dim3(n), dim3(256), 0, s, tm.start, tm.stop, 0, meta, (const T*)q, (const T*)k, \
-                     (const T*)v, cv, layer, inv_freq, Hq, rows_ws, (T*)qws)
+                     (const T*)v, cv, layer, rope, Hq, rows_ws, (T*)qws)
   if (dtype == 0) { if (cv.head_dim == 64) RA(float, 64); else RA(float, 128); }
   else { if (cv.head_dim == 64) RA(bf16_t, 64); else RA(bf16_t, 128); }
 #undef RA
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? 0 : (int)e;
+}
+
+// (cos, sin) of p * w_i for every position p < n_pos and pair i < half: the
+// float64 angle and float64 cos/sin of the definition, rounded to fp32 (the
+// same values a kernel computing them itself would use)
+__global__ void __launch_bounds__(256) rope_table_kernel(const double* __restrict__ inv_freq, int half, int64_t n,
+                                                         float2* __restrict__ tab) {
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= n) return;
+  const int64_t p = idx / half;
+  const int i = (int)(idx % half);
+  float c, sn;
+  rope_cs((double)p, inv_freq[i], &c, &sn);
+  tab[idx] = make_float2(c, sn);
+}
+
+int launch_rope_table(const double* inv_freq, int half, int n_pos, float2* tab, hipStream_t s) {
+  const int64_t n = (int64_t)n_pos * half;
+  if (n == 0) return 0;
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, inv_freq, half, n, tab);
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

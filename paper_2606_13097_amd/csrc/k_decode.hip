@@ -62,7 +62,7 @@ __device__ __forceinline__ float lanes_sum_stride(float x) {
 template <typename T, int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* __restrict__ q,
                                                      const T* __restrict__ k, const T* __restrict__ v, CacheView cv,
-                                                     int layer, const double* __restrict__ inv_freq,
+                                                     int layer, const float2* __restrict__ rope,
                                                      T* __restrict__ out, float* __restrict__ part_o,
                                                      float* __restrict__ part_ml, int* __restrict__ count) {
   constexpr int VEC = Store<T>::VEC;
@@ -87,15 +87,17 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
 
   const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
   const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
+  const int npage = PAGED ? args.new_page[i] : -1;  // a page this step maps, by value
   const int nsplit = args.split0[i + 1] - slot0;
   const int sk = args.split_keys;
   const T* ck = reinterpret_cast<const T*>(cv.k);
   const T* cvv = reinterpret_cast<const T*>(cv.v);
   // every kernel argument in one batch of scalar loads before the first branch
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
-               "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
+               "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(rope),
                "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
+  if (PAGED)
+    asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap), "s"(npage));
   if (split >= nsplit) return;  // padding split of a shorter sequence
 
   const int Hkv = cv.n_kv_heads;
@@ -126,7 +128,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   // rotary frequency, raw query rows, new key (dims and partner dims) and
   // value, then two chunks of cached keys (a chunk past the range re-reads
   // its last key: one row, cached)
-  const double wfreq = inv_freq[t % HALF];
+  const float2 cs_pos = rope[(int64_t)pos * HALF + t % HALF];  // (cos, sin) of the position
   uint4 qa[G][NV], qb[G][NV], na[NV], nb[NV], nvv[NV];
 #pragma unroll
   for (int j = 0; j < G; ++j)
@@ -149,7 +151,10 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   uint4 kr0[U][NV], vr0[U][NV], kr1[U][NV], vr1[U][NV];
   load_chunk(k0, kr0, vr0);
   load_chunk(k0 + CK, kr1, vr1);
-  if (t < HALF) rope_cs((double)pos, wfreq, &s_cos[t], &s_sin[t]);
+  if (t < HALF) {
+    s_cos[t] = cs_pos.x;
+    s_sin[t] = cs_pos.y;
+  }
   __syncthreads();
 
   // rotate lane dims [d0, d0 + DPL) of a row given as (own dims, partner dims)
@@ -262,13 +267,14 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     load_chunk(b + 3 * CK, kr1, vr1);
   }
 
+  if (PAGED && owns_new && hk == 0 && t == 0 && npage >= 0) enter_page(cv, seq, pos, npage);
   if (owns_new && slot == 0) {
     // encode, store and attend the new token (lanes of slot 0)
     float kn[DPL], vn[DPL];
     encode(na, nb, kn);
 #pragma unroll
     for (int nv = 0; nv < NV; ++nv) Store<T>::unpack(nvv[nv], vn + nv * VEC);
-    const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, pos) + d0;
+    const int64_t off = new_token_offset<PAGED>(cv, layer, seq, hk, pos, npage) + d0;
     T* kdst = reinterpret_cast<T*>(cv.k) + off;
     T* vdst = reinterpret_cast<T*>(cv.v) + off;
 #pragma unroll
@@ -351,7 +357,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
 }
 
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml, int* count,
+                  int layer, const float2* rope, int Hq, void* out, float* part_o, float* part_ml, int* count,
                   hipStream_t s, KTime tm) {
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
@@ -359,10 +365,10 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
 #define DK(T, DD, GG)                                                                                       \
   if (cv.page_size)                                                                                         \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,          \
-                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml, count);             \
+                       (const T*)k, (const T*)v, cv, layer, rope, (T*)out, part_o, part_ml, count);             \
   else                                                                                                      \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,         \
-                       (const T*)k, (const T*)v, cv, layer, inv_freq, (T*)out, part_o, part_ml, count)
+                       (const T*)k, (const T*)v, cv, layer, rope, (T*)out, part_o, part_ml, count)
 #define DKG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
     case 1: DK(T, DD, 1); break;                                                                            \

@@ -54,7 +54,7 @@ template <int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const bf16_t* __restrict__ q,
                                                           const bf16_t* __restrict__ k,
                                                           const bf16_t* __restrict__ v, CacheView cv, int layer,
-                                                          const double* __restrict__ inv_freq,
+                                                          const float2* __restrict__ rope,
                                                           bf16_t* __restrict__ out, float* __restrict__ part_o,
                                                           float* __restrict__ part_ml, int* __restrict__ count) {
   static_assert(G >= 1 && G <= 16, "query group");
@@ -81,15 +81,17 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
 
   const int split = blockIdx.x, i = blockIdx.y, hk = blockIdx.z;
   const int seq = args.seq[i], pos = args.pos[i], slot0 = args.split0[i];
+  const int npage = PAGED ? args.new_page[i] : -1;  // a page this step maps, by value
   const int nsplit = args.split0[i + 1] - slot0;
   const int sk = args.split_keys;
   const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
   const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
   // every kernel argument in one batch of scalar loads before the first branch
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
-               "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(inv_freq),
+               "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(rope),
                "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
+  if (PAGED)
+    asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap), "s"(npage));
   if (split >= nsplit) return;  // padding split of a shorter sequence
 
   const int Hkv = cv.n_kv_heads;
@@ -117,7 +119,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   }
 
   // ---- loads, in the order their data is needed
-  const double wfreq = inv_freq[t % HALF];
+  const float2 cs_pos = rope[(int64_t)pos * HALF + t % HALF];  // (cos, sin) of the position
   uint4 qa[KS], qb[KS];  // query head lr (row g - 1 for columns past the group): dims and rotary partners
   {
     const bf16_t* row = q + ((int64_t)i * Hq + hk * G + min(lr, G - 1)) * D;
@@ -172,7 +174,10 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   load_tile(w, kA, vA);
   load_tile(w + 4, kB, vB);
   load_tile(w + 8, kC, vC);
-  if (t < HALF) rope_cs((double)pos, wfreq, &s_cos[t], &s_sin[t]);
+  if (t < HALF) {
+    s_cos[t] = cs_pos.x;
+    s_sin[t] = cs_pos.y;
+  }
   __syncthreads();
 
   // rotate 8 dims d .. d + 7 given (own dims, partner dims), round to bf16
@@ -194,11 +199,12 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
     const uint4 e = encode8(ks * 32 + lq * 8, qa[ks], qb[ks]);
     qB[ks] = lr < G ? e : make_uint4(0u, 0u, 0u, 0u);
   }
+  if (PAGED && owns_new && hk == 0 && t == 0 && npage >= 0) enter_page(cv, seq, pos, npage);
   if (owns_new && t < NDG) {
     // encode the new key, store key and value into the token's cache slot and
     // keep both in LDS for the wave that attends to them
     const uint4 kn = encode8(dn, na, nb);
-    const int64_t off = kv_offset<PAGED>(cv, layer, seq, hk, pos) + dn;
+    const int64_t off = new_token_offset<PAGED>(cv, layer, seq, hk, pos, npage) + dn;
     st16(reinterpret_cast<bf16_t*>(cv.k) + off, kn);
     st16(reinterpret_cast<bf16_t*>(cv.v) + off, nv);
     st16(&s_newk[dn], kn);
@@ -325,7 +331,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
 }
 
 int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                       int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                       int layer, const float2* rope, int Hq, void* out, float* part_o, float* part_ml,
                        int* count, hipStream_t s, KTime tm) {
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
@@ -333,11 +339,11 @@ int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, con
 #define DM(DD, GG)                                                                                            \
   if (cv.page_size)                                                                                           \
     hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, \
-                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, inv_freq, (bf16_t*)out, \
+                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out, \
                           part_o, part_ml, count);                                                            \
   else                                                                                                        \
     hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, \
-                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, inv_freq, (bf16_t*)out, \
+                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out, \
                           part_o, part_ml, count)
 #define DMG(DD)                                                                                               \
   switch (g) {                                                                                                \

@@ -120,7 +120,17 @@ struct DecodeArgs {
   int32_t seq[kMaxDecodeSeqs];
   int32_t pos[kMaxDecodeSeqs];         // the new token's position (= the sequence's length)
   int32_t split0[kMaxDecodeSeqs + 1];  // first partial slot of each sequence; split0[i + 1] - split0[i] splits
+  // paged caches: the physical page this step maps for the new token's logical
+  // page (its first position is the new token), or -1 when the page is mapped
+  // already.  The kernel stores the new token there and enters the page (and
+  // "values not read from the library") into the device page table.
+  int32_t new_page[kMaxDecodeSeqs];
 };
+
+// Rotary table of a cache: for position p and pair i, (cos, sin) of the float64
+// angle p * theta^(-2i/D), each rounded to fp32 -- the values every kernel that
+// encodes a fresh or decoded token at p uses.  [n_pos][D/2] float2.
+int launch_rope_table(const double* inv_freq, int half, int n_pos, float2* tab, hipStream_t s);
 
 int launch_lib_ingest(int dtype, const void* k, const void* v, void* lib_k, void* lib_v, int L, int len,
                       int Hkv, int D, int64_t cap, int64_t tok_off, hipStream_t s);
@@ -140,7 +150,7 @@ int launch_unalias(int dtype, const UnaliasItem* items, int n_items, const void*
 // Encode q and k of n tokens at their positions, store k and v in the cache
 // (layer), write encoded q to qws [Hkv][n * g][D].
 int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, const void* k, const void* v,
-                       const CacheView& cv, int layer, const double* inv_freq, int Hq, void* qws,
+                       const CacheView& cv, int layer, const float2* rope, int Hq, void* qws,
                        hipStream_t s, KTime tm = {});
 
 // By-value work list of one MFMA prefill launch: row blocks (up to 256 query
@@ -182,13 +192,13 @@ int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenM
 // and zero again after it.
 constexpr int kCountStride = 32;
 int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                  int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml, int* count,
+                  int layer, const float2* rope, int Hq, void* out, float* part_o, float* part_ml, int* count,
                   hipStream_t s, KTime tm = {});
 
 // The same step on matrix cores for bf16 caches and query groups of up to 16
 // heads (same arguments; -1 for a group size it has no instance for).
 int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, const void* v, const CacheView& cv,
-                       int layer, const double* inv_freq, int Hq, void* out, float* part_o, float* part_ml,
+                       int layer, const float2* rope, int Hq, void* out, float* part_o, float* part_ml,
                        int* count, hipStream_t s, KTime tm = {});
 
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
