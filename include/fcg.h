@@ -234,6 +234,22 @@ fcg_status fcg_decode(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int
                       const void* q, const void* k, const void* v, void* out,
                       int32_t* positions_out, void* stream);
 
+/* fcg_decode for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, semantics, results and errors as fcg_decode; it calls no
+ * hipMalloc / hipFree and uploads nothing.  Its split partials and arrival
+ * counters live in a static device array of the library (8.5 MiB per GPU,
+ * held until the process ends), not in memory of the cache; the cache itself
+ * must exist already (fcg_cache_create allocates).  Every call on one GPU
+ * shares that array: calls that overlap on one GPU (several streams or host
+ * threads) race.  The first call on a device also launches a small kernel that
+ * zeroes the counters.  Kernel timing (fcg_cache_timing) does not cover it.
+ * Extra errors: EINVAL (more than 64 kv heads), ENOMEM (the step needs more
+ * than 8 MiB of split partials: many long sequences at once; use fcg_decode). */
+fcg_status fcg_decode_noalloc(fcg_cache* cache, int32_t layer, int32_t n_seqs, const int32_t* seqs,
+                              const void* q, const void* k, const void* v, void* out,
+                              int32_t* positions_out, void* stream);
+
 /* ------------------------------------------------------------- diagnostics */
 
 /* ------------------------------------------------- code-cache management */

@@ -39,7 +39,7 @@ LIBS = {
     os.path.join(PKG, "libfcg.so"): [
         os.path.join(CSRC, f) for f in
         ("api.cpp", "planner.cpp", "locality.cpp", "k_graft.hip", "k_append.hip", "k_attn_rows.hip", "k_attn_mfma.hip",
-         "k_decode.hip", "k_decode_mfma.hip")
+         "k_decode.hip", "k_decode_mfma.hip", "noalloc.hip")
     ],
     os.path.join(PKG, "synth", "libfcg_synth.so"): [os.path.join(PKG, "synth", "synth.hip")],
     os.path.join(PKG, "measure", "libfcg_measure.so"): [os.path.join(PKG, "measure", "peak.hip")],

@@ -1177,4 +1177,43 @@ fcg_status fcg_decode(fcg_cache* c, int32_t layer, int32_t n_seqs, const int32_t
   return FCG_OK;
 }
 
+fcg_status fcg_decode_noalloc(fcg_cache* c, int32_t layer, int32_t n_seqs, const int32_t* seqs, const void* q,
+                              const void* k, const void* v, void* out, int32_t* positions_out, void* stream) {
+  if (!c) return fail(FCG_EINVAL, "null cache");
+  if (n_seqs < 0) return fail(FCG_EINVAL, "negative sequence count");
+  if (n_seqs > 0 && !seqs) return fail(FCG_EINVAL, "null sequence array");
+  if (n_seqs > 0 && !c->layout_only() && (!q || !k || !v || !out)) return fail(FCG_EINVAL, "null tensor");
+  if (c->desc.n_kv_heads > kNoAllocMaxKvHeads)
+    return fail(FCG_EINVAL, "fcg_decode_noalloc supports at most " + std::to_string(kNoAllocMaxKvHeads) + " kv heads");
+  std::vector<int32_t> pos;
+  std::vector<std::pair<int32_t, int32_t>> new_pages;
+  std::string msg;
+  if (fcg_status st = c->plan.check_decode(layer, n_seqs, seqs, &pos, &new_pages, &msg)) return fail(st, msg);
+  if (n_seqs == 0) return FCG_OK;
+  const DecodePlan plan = plan_decode(c->desc, n_seqs, pos);
+  const size_t need = (plan.part_o + plan.part_ml) * sizeof(float);
+  if (need > kNoAllocPartBytes)
+    return fail(FCG_ENOMEM, "this step needs " + std::to_string(need) + " bytes of split partials; the static scratch of "
+                                "fcg_decode_noalloc holds " + std::to_string(kNoAllocPartBytes) + " (use fcg_decode)");
+  if (!c->layout_only()) {
+    HIP_TRY(hipSetDevice(c->device), "hipSetDevice");
+    hipStream_t s = (hipStream_t)stream;
+    void* base = nullptr;
+    if (int rc = noalloc_scratch(s, &base)) return hip_fail((hipError_t)rc, "static scratch");
+    c->plan.map_pages(new_pages);
+    const std::vector<int32_t> np = decode_new_pages(c, n_seqs, seqs, pos, new_pages);
+    float* po = reinterpret_cast<float*>(static_cast<char*>(base) + kNoAllocCountBytes);
+    if (fcg_status st = launch_decode_groups(c, layer, n_seqs, seqs, pos, np, plan, q, k, v, out, po,
+                                             po + plan.part_o, static_cast<int32_t*>(base), false, s))
+      return st;
+  } else {
+    c->plan.map_pages(new_pages);
+  }
+  for (int32_t i = 0; i < n_seqs; ++i) {
+    c->plan.mark(seqs[i], layer, pos[i]);
+    if (positions_out) positions_out[i] = pos[i];
+  }
+  return FCG_OK;
+}
+
 }  // extern "C"

@@ -201,6 +201,17 @@ int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, con
                        int layer, const float2* rope, int Hq, void* out, float* part_o, float* part_ml,
                        int* count, hipStream_t s, KTime tm = {});
 
+// Static scratch of the allocation-free decode entry point (noalloc.hip):
+// arrival counters for kMaxDecodeSeqs sequences x kNoAllocMaxKvHeads kv heads,
+// then the split partials.  noalloc_scratch returns its device address on the
+// current device (taken, and the counters zeroed on stream s, at the first call
+// on that device).
+constexpr int kNoAllocMaxKvHeads = 64;
+constexpr size_t kNoAllocCountBytes = (size_t)kMaxDecodeSeqs * kNoAllocMaxKvHeads * kCountStride * sizeof(int32_t);
+constexpr size_t kNoAllocPartBytes = (size_t)8 << 20;
+constexpr size_t kNoAllocScratchBytes = kNoAllocCountBytes + kNoAllocPartBytes;
+int noalloc_scratch(hipStream_t s, void** base);
+
 // Merge split partials into out: part_o fp32 rows, or (mfma_part) bf16 in the
 // accumulator order of the MFMA prefill kernel.
 int launch_combine(int dtype, const CombineArgs& args, const TokenMeta* meta, int Hq, int Hkv, int D,

@@ -36,7 +36,8 @@ EXPORTS = [
     "fcg_lib_host_reserve", "fcg_lib_offload", "fcg_lib_reload", "fcg_lib_segment_state",
     "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_export_v_alias",
     "fcg_cache_device_ptrs",
-    "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_status_string", "fcg_last_error",
+    "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_decode_noalloc", "fcg_status_string",
+    "fcg_last_error",
     "fcg_cache_timing", "fcg_cache_timing_read",
     "fcg_locality_create", "fcg_locality_record", "fcg_locality_set_ppl", "fcg_locality_scores",
     "fcg_locality_residency", "fcg_locality_destroy",
@@ -88,6 +89,7 @@ def _load():
         "fcg_graft": [P, P, I32, P, P, P, P],
         "fcg_patch_prefill": [P, I32, I32, P, P, P, P, P, P, P],
         "fcg_decode": [P, I32, I32, P, P, P, P, P, P, P],
+        "fcg_decode_noalloc": [P, I32, I32, P, P, P, P, P, P, P],
         "fcg_cache_timing": [P, I32],
         "fcg_cache_timing_read": [P, I32, PI32, C.POINTER(C.c_double)],
         "fcg_locality_create": [I32, I32, C.c_double, C.c_double, C.c_double, C.POINTER(P)],
@@ -302,6 +304,15 @@ def fcg_decode(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.
     pos = np.zeros(max(s.size, 1), dtype=np.int32)
     _check(_L.fcg_decode(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
                          pos.ctypes.data, _stream(stream) if q is not None else None))
+    return pos[:s.size]
+
+
+def fcg_decode_noalloc(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.ndarray:
+    """fcg_decode through the entry point that allocates nothing (static device scratch)."""
+    s = _i32(seqs)
+    pos = np.zeros(max(s.size, 1), dtype=np.int32)
+    _check(_L.fcg_decode_noalloc(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v),
+                                 _dptr(out), pos.ctypes.data, _stream(stream) if q is not None else None))
     return pos[:s.size]
 
 
