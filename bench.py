@@ -222,77 +222,128 @@ def locality_update(w, task_ws, reps=200):
             "resident_after": int(keep.sum())}
 
 
-def cpu_baseline(w, task_ws, n_layers_graft=6, n_layers_attn=2):
-    """The oracle, as it stands, on a bounded sample of the same workload."""
+def _cpu_info():
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return model, len(os.sched_getaffinity(0))
+
+
+def _oracle_sample(tw, layers, seq=0, n_dec=2, n_query=None, graft_passes_s=0.0):
+    """Time the oracle's three stages for one sequence of task workload ``tw`` at ``layers``:
+    graft (every grafted segment turned and rounded, values decoded), patch-prefill
+    attention (the first ``n_query`` fresh tokens, or all, as queries over the full cache),
+    and ``n_dec`` decode steps (append, then one query row per head).  Returns seconds and
+    algorithmic work per stage."""
     import numpy as np
     from oracle import attention as oatt, graft as ograft, numerics, rope
     from paper_2606_13097_amd import synth
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:
-        blas_threads = os.cpu_count() or 1
-    sh = w.shape
-    tw = task_ws[0]
+    sh = tw.shape
     winv = rope.inv_freq(sh.head_dim, sh.rope_theta)
-    # graft sample: every grafted segment of one task at n_layers_graft layers
-    inputs = []
-    for layer in range(n_layers_graft):
-        for g, d in zip(tw.graft_seg, tw.graft_dst):
-            inputs.append((int(d) - int(tw.lib_src_pos0[g]), synth.lib_segment(tw, int(g), layer, "k"),
-                           synth.lib_segment(tw, int(g), layer, "v")))
-    # repeat the sample until about 10 s of CPU work have been timed
-    reps, t_graft = 0, 0.0
-    while t_graft < 10.0 and reps < 64:
-        t0 = time.perf_counter()
-        for delta, k, v in inputs:
-            kk = ograft.graft_keys(k, delta, winv, sh.dtype)
-            vv = ograft.graft_values(v, sh.dtype)
-            numerics.encode(kk, sh.dtype), numerics.encode(vv, sh.dtype)
-        t_graft += time.perf_counter() - t0
-        reps += 1
-    graft_bytes = 2 * tw.grafted_tokens * 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes * n_layers_graft * reps
-    # patch-attention sample: the 64 patch tokens at n_layers_attn layers
-    flops = dec_bytes = 0
-    t_att = t_dec = 0.0
-    for layer in range(n_layers_attn):
+    kvb = 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes               # K+V bytes of a token, one layer
+    r = dict(graft_s=0.0, graft_bytes=0, attn_s=0.0, attn_flops=0, dec_s=0.0, dec_bytes=0)
+    m = tw.graft_seq == seq
+    for layer in layers:
         items = [(int(d), int(tw.lib_src_pos0[g]), synth.lib_segment(tw, int(g), layer, "k"),
-                  synth.lib_segment(tw, int(g), layer, "v")) for g, d in zip(tw.graft_seg, tw.graft_dst)]
+                  synth.lib_segment(tw, int(g), layer, "v")) for g, d in zip(tw.graft_seg[m], tw.graft_dst[m])]
+        ntok = sum(k.shape[0] for _, _, k, _ in items)
+        passes, t = 0, 0.0
+        while passes == 0 or t < graft_passes_s:
+            t0 = time.perf_counter()
+            for dst, src, k, v in items:
+                numerics.encode(ograft.graft_keys(k, dst - src, winv, sh.dtype), sh.dtype)
+                numerics.encode(ograft.graft_values(v, sh.dtype), sh.dtype)
+            t += time.perf_counter() - t0
+            passes += 1
+        r["graft_s"] += t
+        r["graft_bytes"] += 2 * ntok * kvb * passes
         K, V, wr = ograft.compose(tw.max_tokens, sh.n_kv_heads, sh.head_dim, items, winv, sh.dtype)
-        pos, rows = tw.fresh_of_seq(0)
-        fq = synth.fresh_tokens(tw, 0, layer, "q", rows)
-        fk = synth.fresh_tokens(tw, 0, layer, "k", rows)
-        fv = synth.fresh_tokens(tw, 0, layer, "v", rows)
-        ograft.place_fresh(K, V, wr, pos, fk, fv, winv, sh.dtype)
-        qe = ograft.encode_fresh(fq, pos, winv, sh.dtype)
+        pos, rows = tw.fresh_of_seq(seq)
+        fq = synth.fresh_tokens(tw, seq, layer, "q", rows)
+        ograft.place_fresh(K, V, wr, pos, synth.fresh_tokens(tw, seq, layer, "k", rows),
+                           synth.fresh_tokens(tw, seq, layer, "v", rows), winv, sh.dtype)
+        nq = len(pos) if n_query is None else min(n_query, len(pos))
+        qe = ograft.encode_fresh(fq[:nq], pos[:nq], winv, sh.dtype)
         t0 = time.perf_counter()
-        oatt.attend(qe, pos, K, V, wr)
-        t_att += time.perf_counter() - t0
-        flops += 4 * sh.n_q_heads * sh.head_dim * int((pos + 1).sum())
-        # decode sample: the first n_dec decode steps (append, then one query row per head)
-        n_dec = min(16, tw.n_decode)
-        dq = synth.decode_tokens(tw, 0, layer, "q", range(n_dec))
-        dk = synth.decode_tokens(tw, 0, layer, "k", range(n_dec))
-        dv = synth.decode_tokens(tw, 0, layer, "v", range(n_dec))
-        for step in range(n_dec):
+        oatt.attend(qe, pos[:nq], K, V, wr)
+        r["attn_s"] += time.perf_counter() - t0
+        r["attn_flops"] += 4 * sh.n_q_heads * sh.head_dim * int((pos[:nq].astype(np.int64) + 1).sum())
+        steps = range(n_dec)
+        dq, dk, dv = (synth.decode_tokens(tw, seq, layer, x, steps) for x in "qkv")
+        for st in steps:
             p = int(np.flatnonzero(wr)[-1]) + 1
             t0 = time.perf_counter()
-            ograft.place_fresh(K, V, wr, [p], dk[step][None], dv[step][None], winv, sh.dtype)
-            oatt.attend_row(ograft.encode_fresh(dq[step][None], [p], winv, sh.dtype)[0], p, K, V, wr)
-            t_dec += time.perf_counter() - t0
-            dec_bytes += (p + 1) * 2 * sh.n_kv_heads * sh.head_dim * sh.elem_bytes
-    return {
-        "value": round(graft_bytes / t_graft / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-        "sample": f"graft of one task's {len(tw.graft_seg)} segments ({tw.grafted_tokens} tokens) at "
-                  f"{n_layers_graft} of {sh.n_layers} layers, {reps} passes: {graft_bytes / 1e6:.1f} MB in "
-                  f"{t_graft:.2f} s (NumPy float64, single thread)",
-        "patch_attn": {"value": round(flops / t_att / 1e12, 6), "unit": "TFLOP/s", "cores": blas_threads,
-                       "sample": f"64 patch tokens x {sh.n_q_heads} heads at {n_layers_attn} layers, "
-                                 f"{flops / 1e9:.2f} GFLOP in {t_att:.2f} s (NumPy float64 + BLAS)"},
-        "decode": {"value": round(dec_bytes / t_dec / 1e9, 4), "unit": "GB/s", "cores": blas_threads,
-                   "sample": f"first {n_dec} decode steps at {n_layers_attn} layers, {dec_bytes / 1e6:.1f} MB of "
-                             f"K/V in {t_dec:.3f} s (NumPy float64)"},
-    }
+            ograft.place_fresh(K, V, wr, [p], dk[st][None], dv[st][None], winv, sh.dtype)
+            oatt.attend_row(ograft.encode_fresh(dq[st][None], [p], winv, sh.dtype)[0], p, K, V, wr)
+            r["dec_s"] += time.perf_counter() - t0
+            r["dec_bytes"] += (p + 1) * kvb
+    return r
+
+
+def _rates(r):
+    return {"graft_gbs": round(r["graft_bytes"] / r["graft_s"] / 1e9, 4) if r["graft_s"] else None,
+            "prefill_attn_tflops": round(r["attn_flops"] / r["attn_s"] / 1e12, 6) if r["attn_s"] else None,
+            "decode_gbs": round(r["dec_bytes"] / r["dec_s"] / 1e9, 4) if r["dec_s"] else None}
+
+
+def cpu_baseline(task_ws, seed):
+    """The oracle, as it stands, timed on this host on bounded samples of the workloads.
+
+    The bench workload (7B class): graft of one task's segments at 6 layers (repeated to
+    about 8 s), patch-prefill attention at 2 layers and 16 decode steps at 2 layers, with
+    the BLAS thread pool at every core of this process's affinity and again at 1 thread.
+    The other workloads: one seeded layer (the middle one) of their first sequence,
+    extrapolated to every layer and sequence (the per-layer work is the same shape)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info, threadpool_limits
+    from paper_2606_13097_amd import synth
+    model, cores = _cpu_info()
+    blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    tw = task_ws[0]
+    sh = tw.shape
+    res = {"kind": "oracle", "cpu_model": model, "cores": cores, "blas_threads": blas}
+    main = _oracle_sample(tw, range(6), n_dec=0, graft_passes_s=8.0 / 6)
+    att = _oracle_sample(tw, [0, sh.n_layers - 1], n_dec=16)
+    with threadpool_limits(1):
+        att1 = _oracle_sample(tw, [0, sh.n_layers - 1], n_dec=16)
+    main.update({k: att[k] for k in ("attn_s", "attn_flops", "dec_s", "dec_bytes")})
+    rates, rates1 = _rates(main), _rates(att1)
+    res.update({
+        "value": rates["graft_gbs"], "unit": "GB/s",
+        "sample": (f"7b: graft of one task's {len(tw.graft_seg)} segments ({tw.grafted_tokens} tokens) at 6 of "
+                   f"{sh.n_layers} layers, {main['graft_bytes'] / 1e6:.0f} MB in {main['graft_s']:.1f} s (NumPy "
+                   f"float64; elementwise NumPy runs on one thread); patch-prefill attention of the 64 patch "
+                   f"tokens and 16 decode steps at layers 0 and {sh.n_layers - 1}"),
+        "graft_cores": 1,
+        "per_config": {"7b": {"threads": blas, **rates,
+                              "one_thread": {k: v for k, v in rates1.items() if k != "graft_gbs"}}},
+    })
+    # the other workloads: one layer of one sequence each, extrapolated
+    for name, kw in (("tiny", {}), ("long16k", {}), ("batched", {}), ("34b", dict(n_query=64))):
+        ow = synth.workload(name, seed=seed, n_decode=2)
+        L = ow.shape.n_layers
+        t0 = time.perf_counter()
+        r = _oracle_sample(ow, [L // 2], n_dec=2, **kw)
+        wall = time.perf_counter() - t0
+        # full-workload work of these stages: every layer, every sequence, all patch tokens
+        kvb = 2 * ow.shape.n_kv_heads * ow.shape.head_dim * ow.shape.elem_bytes
+        full_graft = 2 * ow.grafted_tokens * kvb * L
+        full_flops = 4 * ow.shape.n_q_heads * ow.shape.head_dim * float((ow.fresh_pos.astype(np.int64) + 1).sum()) * L
+        rt = _rates(r)
+        res["per_config"][name] = {
+            "threads": blas, **rt, "extrapolated": L > 1 or ow.n_seqs > 1,
+            "sample": f"layer {L // 2} of {L}, sequence 0 of {ow.n_seqs}"
+                      + (f", {kw['n_query']} of {int((ow.fresh_seq == 0).sum())} patch queries" if kw else "")
+                      + f"; {wall:.1f} s wall including input generation",
+            "full_graft_s": round(full_graft / (rt["graft_gbs"] * 1e9), 2),
+            "full_prefill_attn_s": round(full_flops / (rt["prefill_attn_tflops"] * 1e12), 2)}
+    return res
 
 
 def main():
@@ -587,7 +638,7 @@ def main():
         res["roofline_patch_attn"]["counter_tflops"] = round(cf / (a_kms / 1e3 / (K * sh.n_layers)) / 1e12, 3)
     if not args.no_cpu_baseline:
         log("bench: timing the CPU oracle on a sample")
-        res["cpu_baseline"] = cpu_baseline(w, task_ws)
+        res["cpu_baseline"] = cpu_baseline(task_ws, args.seed)
     setup.close()
     print(json.dumps(res), flush=True)
 

@@ -867,6 +867,22 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     }
     return rb;
   };
+  // bf16 calls whose tokens form, per sequence, one run of consecutive
+  // positions given at consecutive caller indices (a patch span following its
+  // context) run as one fused kernel: it encodes the queries itself, reads the
+  // fresh keys and values from the caller's arrays and stores them into the
+  // cache.  Other calls encode and append first (rope_append).
+  std::vector<std::pair<int32_t, int32_t>> seq_first(d.dtype == FCG_BF16 ? n : 0);  // per rank: (f0, ftok0)
+  bool fused = mfma;
+  for (int r0 = 0; fused && r0 < n;) {
+    int r1 = r0;
+    while (r1 < n && meta[r1].seq == meta[r0].seq) {
+      if (meta[r1].pos != meta[r0].pos + (r1 - r0) || meta[r1].tok != meta[r0].tok + (r1 - r0)) fused = false;
+      seq_first[r1] = {meta[r0].pos, meta[r0].tok};
+      ++r1;
+    }
+    r0 = r1;
+  }
   std::vector<std::pair<int, int>> rblocks = row_blocks(mfma ? std::max(1, 256 / g) : 1);
   // MFMA: unless 256-row blocks alone fill the chip twice, use 128-row blocks
   // of 4 waves sized to run two per CU (one block's softmax beside the other's
@@ -916,7 +932,8 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     const int nsplit = (int)((kend + span - 1) / span);
     const int part0 = nsplit > 1 ? n_part : -1;
     if (nsplit > 1) comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit});
-    pf_rb.push_back(PrefillRb{rb.first, rb.second, meta[rb.first].seq, meta[rb.first].pos, kend - 1, part0});
+    pf_rb.push_back(PrefillRb{rb.first, rb.second, meta[rb.first].seq, meta[rb.first].pos, kend - 1, part0,
+                              mfma ? seq_first[rb.first].first : 0, mfma ? seq_first[rb.first].second : 0});
     pf_nsplit.push_back(nsplit);
     for (int sidx = 0; sidx < nsplit; ++sidx)
       items.push_back(AttnItem{rb.first, rb.second, meta[rb.first].seq, (int)(sidx * span),
@@ -950,7 +967,8 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   const int stride_rows = mfma ? (max_rows > 128 ? 256 : 128) : g;  // pair: max_rows <= 128
   // workspaces first: a failure here leaves the layout untouched
   const size_t qbytes = (size_t)d.n_kv_heads * n * g * d.head_dim * esize(d.dtype);
-  if (fcg_status st = grow(&c->qws, &c->qws_bytes, qbytes, "query workspace")) return st;
+  if (!fused)
+    if (fcg_status st = grow(&c->qws, &c->qws_bytes, qbytes, "query workspace")) return st;
   const size_t po = (size_t)n_part * d.n_kv_heads * stride_rows * d.head_dim;
   const size_t pml = (size_t)n_part * d.n_kv_heads * stride_rows * 2;
   if (n_part)
@@ -967,18 +985,24 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   const CacheView cv = c->view();
   // timing: the append kernel opens the call's interval, the attention
   // launches bracket their own, the last kernel closes the call's
-  const hipEvent_t e_call0 = timing_event(c), e_attn0 = timing_event(c), e_attn1 = timing_event(c);
+  const hipEvent_t e_attn0 = timing_event(c), e_attn1 = timing_event(c);
+  const hipEvent_t e_call0 = fused ? e_attn0 : timing_event(c);
   const hipEvent_t e_call1 = comb.empty() ? e_attn1 : timing_event(c);
-  int rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_rope, d.n_q_heads, c->qws, s,
-                              KTime{e_call0, nullptr});
-  if (rc) return hip_fail((hipError_t)rc, "append launch");
+  int rc = 0;
+  if (!fused) {
+    rc = launch_rope_append(d.dtype, dmeta, n, q, k, v, cv, layer, c->d_rope, d.n_q_heads, c->qws, s,
+                            KTime{e_call0, nullptr});
+    if (rc) return hip_fail((hipError_t)rc, "append launch");
+  }
+  FusedIn fin;
+  if (fused) fin = FusedIn{q, k, v, c->d_rope};
   float* part_o = c->part;
   float* part_ml = c->part ? c->part + po : nullptr;
   if (mfma) {
     for (size_t li = 0; li < pf_launch.size(); ++li) {
       const KTime tm{li == 0 ? e_attn0 : nullptr, li + 1 == pf_launch.size() ? e_attn1 : nullptr};
       rc = launch_attn_mfma(pf_launch[li], dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml,
-                            stride_rows, nbuf, s, tm);
+                            stride_rows, nbuf, s, tm, fin);
       if (rc) break;
     }
   } else

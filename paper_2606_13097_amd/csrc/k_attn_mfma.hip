@@ -104,16 +104,18 @@ __device__ __forceinline__ uint2 ld_tr8(const bf16_t* p) {
 // beside the other's matrix work).  4-wave blocks aim at 256 registers per
 // lane (two waves per SIMD); the four-tile ring at D 128 still needs more,
 // and the compiler keeps its accumulators in AGPRs.
-template <int D, bool PAGED, int WAVES, int NBUF>
+template <int D, bool PAGED, int WAVES, int NBUF, bool FUSED>
 __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
-    float* __restrict__ part_ml, int part_stride_rows) {
+    float* __restrict__ part_ml, int part_stride_rows, const bf16_t* __restrict__ raw_q,
+    const bf16_t* __restrict__ raw_k, const bf16_t* __restrict__ raw_v, const float2* __restrict__ rope) {
   constexpr int NT = WAVES * 64;                    // lanes per block
   constexpr int KS = D / 32;                        // 32-deep k steps over the head dimension
   constexpr int DT = D / 16;                        // 16-wide output tiles over the head dimension
   using Tile = PrefillTile<D>;
   constexpr int NC = Tile::NC;
+  constexpr int HALF = D / 2;
   constexpr int DPT = 2 * NC / WAVES;               // LDS loads per wave per tile (1 KB each)
   static_assert(NC % WAVES == 0, "tile loads split evenly over the waves");
   constexpr int kNBuf = NBUF;
@@ -158,6 +160,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
                "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(Hkv),
                "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
   if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
+  if (FUSED) asm volatile("" ::"s"(rb.f0), "s"(rb.ftok0), "s"(rb.pmax), "s"(raw_q), "s"(raw_k), "s"(raw_v), "s"(rope));
   if (split >= args.n_split || k0 >= kend) return;  // past the last group; padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
@@ -182,16 +185,40 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // one load row 0 and are never written)
   int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
   uint4 qf[2][KS];
+  // fused: the raw query dims of the lane (and their rotary partners) and the
+  // (cos, sin) of its pair indices (lq * 8 + 32 j .. + 7, j < D / 64) at the
+  // row's position; encoded after the first tiles are in flight
+  constexpr int NCS = FUSED ? D / 64 : 1;
+  uint4 qa[2][FUSED ? KS : 1], qb[2][FUSED ? KS : 1], qcs[2][NCS][4];
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int r = 32 * w + 16 * rt + lr;
     const int rl = r < rows ? r : 0;
-    const TokenMeta m = meta[rb.rank0 + rl / g];
-    rpos[rt] = m.pos;
-    rtok[rt] = m.tok;
+    if constexpr (FUSED) {
+      // the block's tokens are consecutive positions from rmin, consecutive caller indices
+      const int tr = rl / g;
+      rpos[rt] = rb.rmin + tr;
+      rtok[rt] = rb.ftok0 + (rb.rmin - rb.f0) + tr;
+      const bf16_t* row = raw_q + ((int64_t)rtok[rt] * Hq + hk * g + rl % g) * D;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)rb.rank0 * g + rl) * D + ks * 32 + lq * 8);
+      for (int ks = 0; ks < KS; ++ks) {
+        const int d = ks * 32 + lq * 8;
+        qa[rt][ks] = ld16(row + d);
+        qb[rt][ks] = ld16(row + (d < HALF ? d + HALF : d - HALF));
+      }
+#pragma unroll
+      for (int j = 0; j < NCS; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          qcs[rt][j][e] = ld16(rope + (int64_t)rpos[rt] * HALF + 32 * j + lq * 8 + 2 * e);
+    } else {
+      const TokenMeta m = meta[rb.rank0 + rl / g];
+      rpos[rt] = m.pos;
+      rtok[rt] = m.tok;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)rb.rank0 * g + rl) * D + ks * 32 + lq * 8);
+    }
   }
 
   // contiguous caches address a head's rows from one base with 32-bit offsets
@@ -234,7 +261,11 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       const int r = slot / NC, pos = slot % NC;
       const int p = min(kb + r, kend - 1);
       const int c = pos ^ (isv ? Tile::swz_v(r) : Tile::swz_k(r));
-      const bf16_t* src = (isv ? vrow(p) : krow(p)) + c * 8;
+      const bf16_t* src;
+      if (FUSED && p >= rb.f0)  // a fresh token: its raw row from the caller's input (keys turned below)
+        src = (isv ? raw_v : raw_k) + ((int64_t)(rb.ftok0 + p - rb.f0) * Hkv + hk) * D + c * 8;
+      else
+        src = (isv ? vrow(p) : krow(p)) + c * 8;
       dma16(src, lds_addr(isv ? B.v : B.k) + jj * 1024);
     }
   };
@@ -254,6 +285,24 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 #pragma unroll
   for (int i = 0; i < kNBuf - 1; ++i)
     if (i < ntiles) issue_to(i, tiles[i]);
+  if constexpr (FUSED) {
+    // encode the queries at their positions (rotate-half pairs, fp32 turn,
+    // rounded to bf16), as the append kernel does
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int d = ks * 32 + lq * 8;
+        const float* cs = reinterpret_cast<const float*>(&qcs[rt][(d % HALF) / 32][0]);  // (cos, sin) x 8
+        float a[8], b[8], y[8];
+        Store<bf16_t>::unpack(qa[rt][ks], a);
+        Store<bf16_t>::unpack(qb[rt][ks], b);
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+          y[e] = d < HALF ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1]) : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
+        qf[rt][ks] = Store<bf16_t>::pack(y);
+      }
+  }
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
 #pragma unroll
@@ -272,6 +321,42 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     if (ahead >= 2) wait_vm<2 * DPT>();
     else if (ahead == 1) wait_vm<DPT>();
     else wait_vm<0>();
+    if constexpr (FUSED) {
+      // keys of fresh tokens arrived raw: turn them in place.  Lane l's chunk c
+      // of row r and its rotary partner c ^ NC/2 (lane l ^ NC/2, same
+      // instruction) both came with this wave's loads; the wave reads both
+      // chunks before it writes (LDS executes a wave's instructions in order).
+      const int kb = k0 + tile * kBN;
+      if (kb + kBN > rb.f0 && rb.f0 < kend) {  // the tile holds fresh keys (block-uniform)
+        Tile& W = tiles[buf];
+#pragma unroll
+        for (int u = 0; u < NC / WAVES; ++u) {
+          const int slot = (wu + WAVES * u) * 64 + lane;
+          const int r = slot / NC, cpos = slot % NC;
+          const int p = kb + r;
+          if (p >= rb.f0 && p < kend) {
+            const int c = cpos ^ Tile::swz_k(r);
+            uint4* own = reinterpret_cast<uint4*>(&W.k[slot * 8]);
+            const uint4* par = reinterpret_cast<const uint4*>(&W.k[(slot ^ (NC / 2)) * 8]);
+            const uint4 xa = *own, xb = *par;
+            const uint4* csp = reinterpret_cast<const uint4*>(rope + (int64_t)p * HALF + (c % (NC / 2)) * 8);
+            uint4 cw[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) cw[e] = csp[e];
+            const float* cs = reinterpret_cast<const float*>(cw);
+            float a[8], b[8], y[8];
+            Store<bf16_t>::unpack(xa, a);
+            Store<bf16_t>::unpack(xb, b);
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              y[e] = c < NC / 2 ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1])
+                                : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
+            asm volatile("" ::: "memory");  // both chunks are read before the write
+            *own = Store<bf16_t>::pack(y);
+          }
+        }
+      }
+    }
     // ... and every wave's; every wave is also done with the previous tile,
     // whose buffer the next load reuses
     lds_barrier();
@@ -435,25 +520,59 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       }
     }
   }
+  if constexpr (FUSED) {
+    // the block's own tokens whose positions fall in its split (each fresh
+    // token and kv head has exactly one such block): their keys, turned at
+    // their positions, and their values go into the cache for later calls
+    const int a0 = max(k0, rb.rmin);
+    bf16_t* ckw = reinterpret_cast<bf16_t*>(cv.k);
+    bf16_t* cvw = reinterpret_cast<bf16_t*>(cv.v);
+    for (int idx = t; idx < (kend - a0) * NC; idx += NT) {
+      const int p = a0 + idx / NC, c = idx % NC;
+      const int64_t src = ((int64_t)(rb.ftok0 + p - rb.f0) * Hkv + hk) * D;
+      const uint4 xa = ld16(raw_k + src + c * 8);
+      const uint4 xb = ld16(raw_k + src + (c ^ (NC / 2)) * 8);
+      const uint4 xv = ld16(raw_v + src + c * 8);
+      const uint4* csp = reinterpret_cast<const uint4*>(rope + (int64_t)p * HALF + (c % (NC / 2)) * 8);
+      uint4 cw[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) cw[e] = csp[e];
+      const float* cs = reinterpret_cast<const float*>(cw);
+      float a[8], b[8], y[8];
+      Store<bf16_t>::unpack(xa, a);
+      Store<bf16_t>::unpack(xb, b);
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        y[e] = c < NC / 2 ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1]) : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
+      const int64_t off = kv_offset<PAGED>(cv, layer, rb.seq, hk, p) + c * 8;
+      st16(ckw + off, Store<bf16_t>::pack(y));
+      st16(cvw + off, xv);
+    }
+  }
 }
 
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm) {
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm, FusedIn fin) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   const int groups = args.n_split * cv.n_kv_heads;  // (split, kv head) pairs
   const dim3 grid = args.xcd_group ? dim3(kXcds * args.n_rb, (groups + kXcds - 1) / kXcds)
                                    : dim3(args.n_rb, args.n_split, cv.n_kv_heads);
   const int waves = part_stride_rows / 32;      // rows per block / 32
   if ((nbuf != 2 && nbuf != 4) || (nbuf == 2 && waves != 4)) return (int)hipErrorInvalidValue;
-#define PF(DD, PG, WV, NB)                                                                                  \
-  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB>), grid, dim3(WV * 64), 0, s, tm.start, tm.stop, 0, args, meta, \
-                     (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out, part_o, part_ml, part_stride_rows)
-#define PFW(DD, PG) { if (nbuf == 2) PF(DD, PG, 4, 2); else if (waves == 8) PF(DD, PG, 8, 4); else PF(DD, PG, 4, 4); }
+  const bool fused = fin.q != nullptr;
+#define PF(DD, PG, WV, NB, FU)                                                                                \
+  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB, FU>), grid, dim3(WV * 64), 0, s, tm.start,   \
+                        tm.stop, 0, args, meta, (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out,       \
+                        part_o, part_ml, part_stride_rows, (const bf16_t*)fin.q, (const bf16_t*)fin.k,          \
+                        (const bf16_t*)fin.v, fin.rope)
+#define PFS(DD, PG, FU) { if (nbuf == 2) PF(DD, PG, 4, 2, FU); else if (waves == 8) PF(DD, PG, 8, 4, FU); else PF(DD, PG, 4, 4, FU); }
+#define PFW(DD, PG) { if (fused) PFS(DD, PG, true) else PFS(DD, PG, false) }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }
   else { if (paged) PFW(64, true) else PFW(64, false) }
 #undef PFW
+#undef PFS
 #undef PF
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;

@@ -158,11 +158,17 @@ int launch_rope_append(int dtype, const TokenMeta* meta, int n, const void* q, c
 // positions (splits past a row block's last position are empty).  The grid is
 // (row block, split, kv head), so a block finds its work without a memory
 // round trip.
-constexpr int kPfMaxRb = 128;
+constexpr int kPfMaxRb = 96;
 struct PrefillRb {
   int32_t rank0, n_rank, seq;
   int32_t rmin, pmax;  // smallest and largest query position of the block
   int32_t part0;       // first partial slot, -1 when the block has a single split
+  // fused launches (fresh tokens encoded and appended by the attention kernel):
+  // the sequence's first fresh position of the call and the caller's index of
+  // that token.  Every position p >= f0 of the sequence up to its last query
+  // is fresh, at caller index ftok0 + (p - f0); the block's own tokens are the
+  // positions rmin .. pmax.
+  int32_t f0, ftok0;
 };
 struct PrefillArgs {
   int32_t n_rb, n_split, span;
@@ -173,9 +179,20 @@ struct PrefillArgs {
 // bf16 MFMA attention of query-workspace rows over the cache.  Blocks of
 // part_stride_rows / 32 waves; nbuf: tiles of the LDS ring, 2 for 4-wave
 // blocks sized to run two per CU, else 4.
+// Fused launches take the caller's fresh q [n][Hq][D], k, v [n][Hkv][D] and the
+// cache's rotary table instead of the query workspace: queries are encoded in
+// the kernel's prologue, fresh keys and values are read from the inputs (keys
+// turned in LDS), and the block owning a fresh token stores its key and value
+// into the cache.  q == nullptr: the workspace path (rope_append ran before).
+struct FusedIn {
+  const void* q = nullptr;
+  const void* k = nullptr;
+  const void* v = nullptr;
+  const float2* rope = nullptr;
+};
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm = {});
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm = {}, FusedIn fin = {});
 
 // VALU attention, one token (g query rows) per item; any dtype.
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
