@@ -931,7 +931,9 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     const int kend = meta[rb.first + rb.second - 1].pos + 1;
     const int nsplit = (int)((kend + span - 1) / span);
     const int part0 = nsplit > 1 ? n_part : -1;
-    if (nsplit > 1) comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit});
+    // fused calls: the output tokens follow from by-value fields, nothing is read from meta
+    const int tok0 = fused ? seq_first[rb.first].second + (meta[rb.first].pos - seq_first[rb.first].first) : -1;
+    if (nsplit > 1) comb.push_back(CombineItem{rb.first, rb.second, n_part, nsplit, tok0});
     pf_rb.push_back(PrefillRb{rb.first, rb.second, meta[rb.first].seq, meta[rb.first].pos, kend - 1, part0,
                               mfma ? seq_first[rb.first].first : 0, mfma ? seq_first[rb.first].second : 0});
     pf_nsplit.push_back(nsplit);
@@ -976,12 +978,16 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   Blob blob;
   std::vector<std::pair<int32_t, size_t>> rows;
   stage_pages(c, new_pages, &blob, &rows);
-  const size_t o_meta = blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
+  // fused calls take their whole plan by value: an upload (one more copy
+  // before the kernel) only when the call maps new pages
+  const bool upload_plan = !fused || !rows.empty();
+  const size_t o_meta = fused ? 0 : blob.add(meta.data(), meta.size() * sizeof(TokenMeta));
   const size_t o_items = mfma ? 0 : blob.add(items.data(), items.size() * sizeof(AttnItem));
-  char* dev;
-  size_t off;
-  if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
-  const TokenMeta* dmeta = (const TokenMeta*)(dev + o_meta);
+  char* dev = nullptr;
+  size_t off = 0;
+  if (upload_plan)
+    if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  const TokenMeta* dmeta = fused ? nullptr : (const TokenMeta*)(dev + o_meta);
   const CacheView cv = c->view();
   // timing: the append kernel opens the call's interval, the attention
   // launches bracket their own, the last kernel closes the call's
@@ -1027,7 +1033,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   }
   time_open(c, FCG_TIME_PREFILL, e_call0);
   time_close(c, FCG_TIME_PREFILL, e_call1);
-  return c->ring.retire(off, blob.bytes.size(), s);
+  return upload_plan ? c->ring.retire(off, blob.bytes.size(), s) : FCG_OK;
 }
 
 // Split plan of one decode call: split length in keys and the largest number

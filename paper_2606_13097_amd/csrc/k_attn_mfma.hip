@@ -245,6 +245,13 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     }
     return v_row<true, bf16_t>(cv, layer, rb.seq, hk, p);
   };
+  // the cache's own value row of position p (fresh tokens' pages are never read from the library)
+  auto vown = [&](int p) -> const bf16_t* {
+    if (!PAGED) return vbase + p * D;
+    if (window)
+      return cvv + (int64_t)layer * cv.layer_stride + (((int64_t)s_pg[(p >> 4) - lpa] * Hkv + hk) * 16 + (p & 15)) * D;
+    return cvv + kv_offset<true>(cv, layer, rb.seq, hk, p);
+  };
   // This wave's share of tile `tile` into its ring buffer: instruction j of
   // the tile (K: 0 .. NC - 1, V: NC .. 2 NC - 1) fills slots 64 j' .. 64 j' + 63
   // of the K or V rows, lane l the slot of row (64 j' + l) / NC at chunk
@@ -340,19 +347,43 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
             const uint4* par = reinterpret_cast<const uint4*>(&W.k[(slot ^ (NC / 2)) * 8]);
             const uint4 xa = *own, xb = *par;
             const uint4* csp = reinterpret_cast<const uint4*>(rope + (int64_t)p * HALF + (c % (NC / 2)) * 8);
-            uint4 cw[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) cw[e] = csp[e];
-            const float* cs = reinterpret_cast<const float*>(cw);
-            float a[8], b[8], y[8];
+            float a[8], b[8];
+            uint32_t yw[4];
             Store<bf16_t>::unpack(xa, a);
             Store<bf16_t>::unpack(xb, b);
 #pragma unroll
-            for (int e = 0; e < 8; ++e)
-              y[e] = c < NC / 2 ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1])
-                                : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
+            for (int h = 0; h < 2; ++h) {  // four dims at a time: (cos, sin) of pairs i0 + 4h .. + 3
+              const uint4 c0 = csp[2 * h], c1 = csp[2 * h + 1];
+              const float cs[8] = {__uint_as_float(c0.x), __uint_as_float(c0.y), __uint_as_float(c0.z),
+                                   __uint_as_float(c0.w), __uint_as_float(c1.x), __uint_as_float(c1.y),
+                                   __uint_as_float(c1.z), __uint_as_float(c1.w)};
+              float y[4];
+#pragma unroll
+              for (int e = 0; e < 4; ++e) {
+                const int de = 4 * h + e;
+                y[e] = c < NC / 2 ? fmaf(a[de], cs[2 * e], -b[de] * cs[2 * e + 1])
+                                  : fmaf(a[de], cs[2 * e], b[de] * cs[2 * e + 1]);
+              }
+              yw[2 * h] = pack_bf16x2(y[0], y[1]);
+              yw[2 * h + 1] = pack_bf16x2(y[2], y[3]);
+            }
             asm volatile("" ::: "memory");  // both chunks are read before the write
-            *own = Store<bf16_t>::pack(y);
+            const uint4 yk = make_uint4(yw[0], yw[1], yw[2], yw[3]);
+            *own = yk;
+            // the block's own token (exactly one block per fresh token and kv
+            // head): its turned key also goes into the cache for later calls
+            if (p >= rb.rmin) st16(const_cast<bf16_t*>(krow(p)) + c * 8, yk);
+          }
+        }
+        // ... and its value, as it arrived
+#pragma unroll
+        for (int u = NC / WAVES; u < DPT; ++u) {
+          const int slot = (wu + WAVES * u - NC) * 64 + lane;
+          const int r = slot / NC, cpos = slot % NC;
+          const int p = kb + r;
+          if (p >= rb.rmin && p >= rb.f0 && p < kend) {
+            const int c = cpos ^ Tile::swz_v(r);
+            st16(const_cast<bf16_t*>(vown(p)) + c * 8, *reinterpret_cast<const uint4*>(&W.v[slot * 8]));
           }
         }
       }
@@ -518,35 +549,6 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
         part_ml[pr * 2 + 0] = mrow[rt];
         part_ml[pr * 2 + 1] = l;
       }
-    }
-  }
-  if constexpr (FUSED) {
-    // the block's own tokens whose positions fall in its split (each fresh
-    // token and kv head has exactly one such block): their keys, turned at
-    // their positions, and their values go into the cache for later calls
-    const int a0 = max(k0, rb.rmin);
-    bf16_t* ckw = reinterpret_cast<bf16_t*>(cv.k);
-    bf16_t* cvw = reinterpret_cast<bf16_t*>(cv.v);
-    for (int idx = t; idx < (kend - a0) * NC; idx += NT) {
-      const int p = a0 + idx / NC, c = idx % NC;
-      const int64_t src = ((int64_t)(rb.ftok0 + p - rb.f0) * Hkv + hk) * D;
-      const uint4 xa = ld16(raw_k + src + c * 8);
-      const uint4 xb = ld16(raw_k + src + (c ^ (NC / 2)) * 8);
-      const uint4 xv = ld16(raw_v + src + c * 8);
-      const uint4* csp = reinterpret_cast<const uint4*>(rope + (int64_t)p * HALF + (c % (NC / 2)) * 8);
-      uint4 cw[4];
-#pragma unroll
-      for (int e = 0; e < 4; ++e) cw[e] = csp[e];
-      const float* cs = reinterpret_cast<const float*>(cw);
-      float a[8], b[8], y[8];
-      Store<bf16_t>::unpack(xa, a);
-      Store<bf16_t>::unpack(xb, b);
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        y[e] = c < NC / 2 ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1]) : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
-      const int64_t off = kv_offset<PAGED>(cv, layer, rb.seq, hk, p) + c * 8;
-      st16(ckw + off, Store<bf16_t>::pack(y));
-      st16(cvw + off, xv);
     }
   }
 }

@@ -183,7 +183,7 @@ __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const To
   const int r0 = blockIdx.z * kCombRows;
   const int nr = min(kCombRows, it.n_rank * g - r0);
   const int np = it.n_part;
-  asm volatile("" ::"s"(it.rank0), "s"(nr), "s"(np), "s"(it.part0), "s"(meta), "s"(part_o), "s"(part_ml),
+  asm volatile("" ::"s"(it.rank0), "s"(nr), "s"(np), "s"(it.part0), "s"(it.tok0), "s"(meta), "s"(part_o), "s"(part_ml),
                "s"(out), "s"(Hq), "s"(Hkv), "s"(part_stride_rows));
   if (nr <= 0) return;
   auto prow = [&](int s, int r) { return ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + r0 + r; };
@@ -214,7 +214,7 @@ __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const To
 #pragma unroll
     for (int u = 0; u < kCombPre; ++u) pre[u] = mfma_part(min(u, np - 1), my_r, my_c4);
   }
-  const TokenMeta mt = meta[it.rank0 + (r0 + my_r) / g];
+  const int out_tok = it.tok0 >= 0 ? it.tok0 + (r0 + my_r) / g : meta[it.rank0 + (r0 + my_r) / g].tok;
   for (int idx = t; idx < nr * np; idx += 256) {
     const int r = idx / np, s = idx % np;
     s_f[r][s] = part_ml[prow(s, r) * 2];
@@ -280,7 +280,7 @@ __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const To
       return;
     }
   }
-  T* dst = out + ((int64_t)mt.tok * Hq + hk * g + (r0 + my_r) % g) * D + my_c4 * 4;
+  T* dst = out + ((int64_t)out_tok * Hq + hk * g + (r0 + my_r) % g) * D + my_c4 * 4;
   Store<T>::store1(dst + 0, acc.x);
   Store<T>::store1(dst + 1, acc.y);
   Store<T>::store1(dst + 2, acc.z);

@@ -102,6 +102,7 @@ struct AttnItem {
 struct CombineItem {
   int32_t rank0, n_rank;
   int32_t part0, n_part;  // partial slots part0 .. part0 + n_part - 1
+  int32_t tok0;           // >= 0: the caller's index of rank0's token, the rest consecutive; -1: from meta
 };
 // By-value plan of one combine launch.
 constexpr int kCombMaxItems = 128;
