@@ -185,11 +185,10 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // one load row 0 and are never written)
   int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
   uint4 qf[2][KS];
-  // fused: the raw query dims of the lane (and their rotary partners) and the
-  // (cos, sin) of its pair indices (lq * 8 + 32 j .. + 7, j < D / 64) at the
-  // row's position; encoded after the first tiles are in flight
-  constexpr int NCS = FUSED ? D / 64 : 1;
-  uint4 qa[2][FUSED ? KS : 1], qb[2][FUSED ? KS : 1], qcs[2][NCS][4];
+  // fused: the raw query dims of the lane, encoded after the first tiles are
+  // in flight.  The rotary partner of dims d (d +- D/2) is the lane's own k
+  // step ks ^ (D / 64).
+  uint4 qa[2][FUSED ? KS : 1];
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
     const int r = 32 * w + 16 * rt + lr;
@@ -201,16 +200,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       rtok[rt] = rb.ftok0 + (rb.rmin - rb.f0) + tr;
       const bf16_t* row = raw_q + ((int64_t)rtok[rt] * Hq + hk * g + rl % g) * D;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int d = ks * 32 + lq * 8;
-        qa[rt][ks] = ld16(row + d);
-        qb[rt][ks] = ld16(row + (d < HALF ? d + HALF : d - HALF));
-      }
-#pragma unroll
-      for (int j = 0; j < NCS; ++j)
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-          qcs[rt][j][e] = ld16(rope + (int64_t)rpos[rt] * HALF + 32 * j + lq * 8 + 2 * e);
+      for (int ks = 0; ks < KS; ++ks) qa[rt][ks] = ld16(row + ks * 32 + lq * 8);
     } else {
       const TokenMeta m = meta[rb.rank0 + rl / g];
       rpos[rt] = m.pos;
@@ -289,21 +279,49 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // for those loads here (it waits for every vector load, these tiles
   // included), not inside the loop, where its wait would also drain the
   // prefetched tiles on every pass.
+  // fused: the rotary table rows of the block's tokens (consecutive positions,
+  // so one contiguous run of n_rank * D/2 (cos, sin) pairs) go into the ring
+  // buffer that the prologue leaves free, when they fit; else each lane reads
+  // its pairs from the table
+  const int cs_bytes = FUSED ? rb.n_rank * HALF * 8 : 0;
+  const bool stage_cs = FUSED && cs_bytes <= (int)sizeof(Tile);
+  if (FUSED && stage_cs) {
+    const int nchunk = cs_bytes / 16;  // 16-byte chunks, 64 per instruction
+    const uint4* src = reinterpret_cast<const uint4*>(rope + (int64_t)rb.rmin * HALF);
+    for (int j = wu; j * 64 < nchunk; j += WAVES)
+      dma16(src + min(j * 64 + lane, nchunk - 1), lds_addr(&tiles[kNBuf - 1]) + j * 1024);
+  }
 #pragma unroll
   for (int i = 0; i < kNBuf - 1; ++i)
     if (i < ntiles) issue_to(i, tiles[i]);
   if constexpr (FUSED) {
     // encode the queries at their positions (rotate-half pairs, fp32 turn,
     // rounded to bf16), as the append kernel does
+    if (stage_cs) {
+      wait_vm<0>();  // the table rows (issued first) have landed, and this wave's first tiles
+      lds_barrier();
+    }
+    const uint4* cs_lds = reinterpret_cast<const uint4*>(&tiles[kNBuf - 1]);
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int d = ks * 32 + lq * 8;
-        const float* cs = reinterpret_cast<const float*>(&qcs[rt][(d % HALF) / 32][0]);  // (cos, sin) x 8
+        const int i0 = d % HALF;  // first pair index of the lane's 8 dims
+        uint4 cw[4];
+        if (stage_cs) {
+          const uint4* c4 = cs_lds + (((rpos[rt] - rb.rmin) * HALF + i0) >> 1);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cw[e] = c4[e];
+        } else {
+          const uint4* c4 = reinterpret_cast<const uint4*>(rope + (int64_t)rpos[rt] * HALF + i0);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) cw[e] = c4[e];
+        }
+        const float* cs = reinterpret_cast<const float*>(cw);  // (cos, sin) x 8
         float a[8], b[8], y[8];
         Store<bf16_t>::unpack(qa[rt][ks], a);
-        Store<bf16_t>::unpack(qb[rt][ks], b);
+        Store<bf16_t>::unpack(qa[rt][ks ^ (HALF / 32)], b);
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           y[e] = d < HALF ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1]) : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
