@@ -497,9 +497,9 @@ def main():
         # HBM bytes the attention must move: the visible keys and values once, the
         # encoded queries in and the outputs out
         qo = 2 * len(tw.fresh_pos) * sh.n_q_heads * sh.head_dim * sh.elem_bytes
-        p_bytes += (tw.seq_len_after_prefill(0) * kvb + qo) * sh.n_layers
-        ctx = tw.seq_len_after_prefill(0)
-        d_bytes += sum((ctx + t + 1) * kvb for t in range(tw.n_decode)) * sh.n_layers
+        ctxs = [tw.seq_len_after_prefill(q) for q in range(w.n_seqs)]       # every sequence of the batch
+        p_bytes += (sum(ctxs) * kvb + qo) * sh.n_layers
+        d_bytes += sum((c + t + 1) * kvb for c in ctxs for t in range(tw.n_decode)) * sh.n_layers
         n_dec_calls += tw.n_decode * sh.n_layers
     K = args.steps
     pp_ms = pd_ms = pp_flops = pp_bytes = pd_bytes = 0.0
@@ -509,9 +509,9 @@ def main():
         pd_ms += e1.elapsed_time(e2)
         pp_flops += 4 * sh.n_q_heads * sh.head_dim * float((cpos.astype(np.int64) + 1).sum()) * sh.n_layers
         qo = 2 * len(cpos) * sh.n_q_heads * sh.head_dim * sh.elem_bytes
-        pp_bytes += (int(cpos[cseq == 0].max()) + 1) * kvb * sh.n_layers + qo * sh.n_layers
-        end = int(cpos[cseq == 0].max()) + 1
-        pd_bytes += sum((end + t + 1) * kvb for t in range(n_fim)) * sh.n_layers
+        ends = [int(cpos[cseq == q].max()) + 1 for q in range(w.n_seqs)]
+        pp_bytes += sum(ends) * kvb * sh.n_layers + qo * sh.n_layers
+        pd_bytes += sum((e + t + 1) * kvb for e in ends for t in range(n_fim)) * sh.n_layers
     (_, _), (pna, pa_kms), (npp, pp_kms), (npd, pd_kms), (npda, pda_kms) = (pkt[k] for k in range(5))
     assert pna == npp == K * sh.n_layers and npd == npda == K * sh.n_layers * n_fim, pkt
     (ng, g_kms), (na, a_kms), (npf, p_kms), (nd_, d_kms), (nda, da_kms) = kt[0], kt[1], kt[2], kt[3], kt[4]

@@ -58,7 +58,27 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
   const int t = threadIdx.x;
   const int Hkv = cv.n_kv_heads;
 
-  if (t < HALF) rope_cs((double)ch.delta, inv_freq[t], &s_cos[t], &s_sin[t]);
+  // paged caches: the page-table entries of the run's (at most five) logical
+  // pages, loaded once with the data rather than once per stored row (a
+  // lookup per row put a dependent load in front of every store)
+  constexpr int NPG = PAGED ? (kGraftChunk + 15) / 16 + 1 : 1;
+  int32_t pg[NPG];
+  const int lp0 = ch.dst >> 4;
+  if (PAGED) {
+    const int32_t* prow = cv.page_table + (int64_t)ch.seq * 2 * cv.n_lp + lp0;
+    const int last = ((ch.dst + ch.n - 1) >> 4) - lp0;
+#pragma unroll
+    for (int i = 0; i < NPG; ++i) pg[i] = prow[min(i, last)];
+  }
+  // element offset of (layer l, head h, position pos) in the cache
+  auto dst_off = [&](int pos) -> int64_t {
+    if (!PAGED) return kv_offset<false>(cv, l, ch.seq, h, pos);
+    const int e = (pos >> 4) - lp0;
+    int32_t page = pg[0];
+#pragma unroll
+    for (int i = 1; i < NPG; ++i) page = e == i ? pg[i] : page;
+    return (int64_t)l * cv.layer_stride + (((int64_t)page * Hkv + h) * 16 + (pos & 15)) * D;
+  };
 
   const int64_t src_base = (((int64_t)l * Hkv + h) * cap + ch.src_tok) * D;
   const T* sk = lib_k + src_base;
@@ -89,6 +109,8 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
       vv[p] = ld16_nt(sv + (int64_t)j * D + vc * VEC);
     }
   }
+  // cos/sin of the run's delta, while the loads are in flight
+  if (t < HALF) rope_cs((double)ch.delta, inv_freq[t], &s_cos[t], &s_sin[t]);
   __syncthreads();  // cos/sin ready
 
   float c[VEC], s[VEC];
@@ -109,7 +131,7 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
         y1[e] = fmaf(x1[e], c[e], -x2[e] * s[e]);
         y2[e] = fmaf(x2[e], c[e], x1[e] * s[e]);
       }
-      const int64_t off = kv_offset<PAGED>(cv, l, ch.seq, h, ch.dst + j);
+      const int64_t off = dst_off(ch.dst + j);
       st16(ck + off + kc * VEC, Store<T>::pack(y1));
       st16(ck + off + HALF + kc * VEC, Store<T>::pack(y2));
     }
@@ -120,7 +142,7 @@ __global__ void __launch_bounds__(256) graft_kernel(const GraftChunk* __restrict
     const int j = p * VR + vr;
     const int pg0 = (ch.dst + j) & ~15;
     if (j < ch.n && !(alias && pg0 >= ch.seg_lo && pg0 + 16 <= ch.seg_hi)) {
-      const int64_t off = kv_offset<PAGED>(cv, l, ch.seq, h, ch.dst + j);
+      const int64_t off = dst_off(ch.dst + j);
       st16(cvv + off + vc * VEC, vv[p]);
     }
   }
