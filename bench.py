@@ -605,30 +605,78 @@ def main():
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},
     }
     res["locality"] = locality_update(w, task_ws)
-    # host tier: one task's segments to pinned host memory and back (the cache
-    # is emptied first: a value-aliasing cache pins the segments it reads)
+    # host tier (the DRAM tier of the code cache): one task's grafted segments to pinned
+    # host memory and back, three rounds (the first writes the host slabs for the first
+    # time); then the same offload on a side stream while the next task grafts on the main
+    # stream (the cache is emptied first: a value-aliasing cache pins the segments it reads)
     setup.reset()
     segs = sorted(set(int(g) for g in task_ws[0].graft_seg))
     tokens = sum(int(w.lib_lengths[g]) for g in segs)
-    fcg.fcg_lib_host_reserve(lib, tokens)
-    torch.cuda.synchronize()
-    o0 = ev()
-    for g in segs:
-        fcg.fcg_lib_offload(lib, g, sp)
-    o1 = ev()
-    for g in segs:
-        fcg.fcg_lib_reload(lib, g, sp)
-    o2 = ev()
+    nxt = task_ws[1]
+    used = set(segs) | set(int(x) for x in nxt.graft_seg)
+    off_only = [g for g in range(len(w.lib_lengths)) if g not in used][:len(segs)]
+    fcg.fcg_lib_host_reserve(lib, tokens + sum(int(w.lib_lengths[g]) for g in off_only))
+    side = torch.cuda.Stream()
+    sside = side.cuda_stream
+
+    def sev(st):
+        e = torch.cuda.Event(enable_timing=True)
+        e.record(st)
+        return e
+
     torch.cuda.synchronize()
     tb = tokens * sh.token_bytes
+    rounds = []
+    for _ in range(3):
+        o0 = sev(side)
+        for g in segs:
+            fcg.fcg_lib_offload(lib, g, sside)
+        o1 = sev(side)
+        for g in segs:
+            fcg.fcg_lib_reload(lib, g, sside)
+        o2 = sev(side)
+        torch.cuda.synchronize()
+        rounds.append((o0.elapsed_time(o1), o1.elapsed_time(o2)))
+    # the overlap case offloads segments neither task uses and none offloaded before
+    # (each offload a real copy) while the next task grafts
+    g_alone = []
+    for _ in range(3):
+        for s_ in range(w.n_seqs):
+            fcg.fcg_cache_reset(cache, s_)
+        a0 = ev()
+        fcg.fcg_graft(cache, lib, nxt.graft_seq, nxt.graft_seg, nxt.graft_dst, sp)
+        a1 = ev()
+        torch.cuda.synchronize()
+        g_alone.append(a0.elapsed_time(a1))
+    for s_ in range(w.n_seqs):
+        fcg.fcg_cache_reset(cache, s_)
+    b0, c0 = ev(), sev(side)
+    for g in off_only:
+        fcg.fcg_lib_offload(lib, g, sside)
+    c1 = sev(side)
+    fcg.fcg_graft(cache, lib, nxt.graft_seq, nxt.graft_seg, nxt.graft_dst, sp)
+    b1 = ev()
+    torch.cuda.synchronize()
+    for g in off_only:
+        fcg.fcg_lib_reload(lib, g, sside)
+    torch.cuda.synchronize()
+    ob = sum(int(w.lib_lengths[g]) for g in off_only) * sh.token_bytes
     res["offload_reload"] = {
         "segments": len(segs), "bytes": tb,
-        "offload_ms": round(o0.elapsed_time(o1), 3), "reload_ms": round(o1.elapsed_time(o2), 3),
-        "offload_gbs": round(tb / (o0.elapsed_time(o1) / 1e3) / 1e9, 2),
-        "reload_gbs": round(tb / (o1.elapsed_time(o2) / 1e3) / 1e9, 2),
-        "note": "one task's grafted segments (all layers, K and V) to pinned host slabs and back, "
-                "including the call overhead; the paper's RTX 4090 figures per synthesis are 20.33 ms "
-                "(GPU to host) and 23.42 ms (host to GPU)"}
+        "offload_ms": [round(r[0], 3) for r in rounds], "reload_ms": [round(r[1], 3) for r in rounds],
+        "offload_gbs": round(tb / (rounds[0][0] / 1e3) / 1e9, 2),
+        "offload_again_ms": "segments keep their host copy: later offloads only free the device range",
+        "reload_gbs": round(tb / (float(np.median([r[1] for r in rounds[1:]])) / 1e3) / 1e9, 2),
+        "overlap": {"offloaded_segments": len(off_only), "offloaded_bytes": ob,
+                    "offload_ms_side_stream": round(c0.elapsed_time(c1), 3),
+                    "offload_gbs_side_stream": round(ob / (c0.elapsed_time(c1) / 1e3) / 1e9, 2),
+                    "graft_ms_alone": round(float(np.median(g_alone)), 3),
+                    "graft_ms_beside_offload": round(b0.elapsed_time(b1), 3)},
+        "note": "one task's grafted segments (all layers, K and V) to pinned host slabs and back on a side "
+                "stream, one strided copy per segment and tensor (three rounds; the first offload copies, later "
+                "ones only free the device range); 'overlap' offloads as many other segments, never offloaded "
+                "before, while the next task grafts on the main stream. The paper's RTX 4090 figures per synthesis are 20.33 ms (GPU to host) and 23.42 ms "
+                "(host to GPU)"}
     res["copy_ceiling"] = copy_ceiling(int(round(g_bytes / K)), graft_gbs)
     res["mfma_ceiling"] = mfma_ceiling(attn_tflops)
     res["mfma_ceiling"]["issue_rate"] = mfma_rate(0)

@@ -105,6 +105,28 @@ fcg_status fcg_lib_create(const fcg_model_desc* desc, int64_t capacity_tokens,
 fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, const void* k,
                                const void* v, void* stream, int32_t* seg_id);
 
+/* The update step of the cache management (Alg. 1; Sec. 4.1: low-scored
+ * entries go to DRAM, high-scored ones stay on the GPU): with loc tracking one
+ * function per library segment (function id = segment id), decide which
+ * segments stay in device memory and move the others: segments read in place
+ * by an FCG_ALIAS_V cache stay; then, in descending locality score (Eq. 3),
+ * a segment stays while its bytes (len x K+V of all layers) fit in
+ * budget_bytes; with ppl_threshold > 0 (the hyperparameter table's
+ * perplexity-based eviction threshold, 15.0) segments whose perplexity is
+ * below it are placed only after all others.  budget_bytes < 0 takes the
+ * table's GPU memory threshold: 0.85 of the device memory less a 2 GB reserve
+ * less what the rest of the process holds (at most the slabs).  Offloads are
+ * issued first, then reloads, all on stream (a side stream is fine: grafts
+ * wait for reloads, and reused ranges wait for earlier grafts).
+ * *n_offloaded / *n_reloaded (host, may be NULL) receive the moves.
+ * Errors: EINVAL (null arguments, loc's size differs from the segment count,
+ * negative threshold), ESTATE (an offload without a host tier), ENOMEM (host
+ * tier full, or no device range for a reload: the state stays consistent, the
+ * moves made so far remain). */
+fcg_status fcg_lib_update_residency(fcg_lib* lib, const fcg_locality* loc, int64_t budget_bytes,
+                                    double ppl_threshold, void* stream, int32_t* n_offloaded,
+                                    int32_t* n_reloaded);
+
 /* Where segment seg_id sits: tokens tok_off .. tok_off + len - 1 of every
  * [Hkv][capacity][D] slab (tok_off = -1 while offloaded); keys encoded from
  * src_pos0.  Any output may be NULL. */

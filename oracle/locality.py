@@ -26,7 +26,15 @@ Readings where the paper leaves a choice:
   - residency (Alg. 1, the update step): functions in descending score, ties
     by ascending id, are kept on the GPU while their summed cost fits the
     budget; a function that does not fit is skipped and later ones are still
-    considered.
+    considered;
+  - the perplexity-based eviction threshold tau of the hyperparameter table
+    (App. B.2, 15.0): functions whose perplexity is below tau -- code the model
+    already predicts well, where the semantic term gives the least -- leave the
+    GPU first.  Functions at or above tau are placed first (in score order),
+    then the others (in score order) in what remains; tau = 0 leaves the plain
+    score order;
+  - entries that must stay on the GPU (read in place by a cache) are kept
+    before anything else and their cost is counted first.
 """
 from __future__ import annotations
 
@@ -109,13 +117,21 @@ class Locality:
             out[f] = (1.0 - cur[f]) * mix + cur[f]
         return out
 
-    def residency(self, budget: int, cost: Sequence[int]) -> np.ndarray:
+    def residency(self, budget: int, cost: Sequence[int], tau: float = 0.0, pinned=None) -> np.ndarray:
         s = self.scores()
-        order = sorted(range(self.n), key=lambda f: (-s[f], f))
         keep = np.zeros(self.n, dtype=np.uint8)
         used = 0
-        for f in order:
-            if used + int(cost[f]) <= budget:
+        pinned = np.zeros(self.n, dtype=bool) if pinned is None else np.asarray(pinned, dtype=bool)
+        for f in range(self.n):
+            if pinned[f]:
                 keep[f] = 1
                 used += int(cost[f])
+        order = sorted(range(self.n), key=lambda f: (-s[f], f))
+        groups = [[f for f in order if self.ppl[f] >= tau], [f for f in order if self.ppl[f] < tau]] \
+            if tau > 0 else [order]
+        for group in groups:
+            for f in group:
+                if not keep[f] and used + int(cost[f]) <= budget:
+                    keep[f] = 1
+                    used += int(cost[f])
         return keep

@@ -17,6 +17,7 @@
 #include "errors.hpp"
 #include "fcg.h"
 #include "kernels.hpp"
+#include "locality.hpp"
 #include "planner.hpp"
 
 using namespace fcg;
@@ -177,6 +178,12 @@ struct fcg_lib {
   void* host_k = nullptr;
   void* host_v = nullptr;
   hipEvent_t freed = nullptr;  // after the copies that read the last freed device range
+  // Ordering across streams (offload / reload on a side stream beside grafts):
+  // a graft waits for the last reload; a reload or an ingest into a freed
+  // range waits for the last graft (which may still read that range) and the
+  // offload that freed it.
+  mutable hipEvent_t graft_done = nullptr;
+  hipEvent_t reload_done = nullptr;
 
   // first fit among freed ranges, else past the high-water mark; -1 if nothing fits
   int64_t alloc(int64_t len) {
@@ -418,6 +425,12 @@ fcg_status fcg_lib_create(const fcg_model_desc* desc, int64_t capacity_tokens, i
     delete lib;
     return fail(FCG_ENOMEM, "library slabs do not fit in device memory");
   }
+  if (hipEventCreateWithFlags(&lib->freed, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&lib->graft_done, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&lib->reload_done, hipEventDisableTiming) != hipSuccess) {
+    fcg_lib_destroy(lib);
+    return fail(FCG_EHIP, "hipEventCreate");
+  }
   *out = lib;
   return FCG_OK;
 }
@@ -437,7 +450,11 @@ fcg_status fcg_lib_add_segment(fcg_lib* lib, int32_t len, int32_t src_pos0, cons
   if (!(lib->flags & FCG_LAYOUT_ONLY)) {
     HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
     // a range an offload freed is written only after that offload has read it
-    if (reuse && lib->freed) HIP_TRY(hipStreamWaitEvent((hipStream_t)stream, lib->freed, 0), "hipStreamWaitEvent");
+    // and after the last graft (which may have read it) has run
+    if (reuse) {
+      HIP_TRY(hipStreamWaitEvent((hipStream_t)stream, lib->freed, 0), "hipStreamWaitEvent");
+      HIP_TRY(hipStreamWaitEvent((hipStream_t)stream, lib->graft_done, 0), "hipStreamWaitEvent");
+    }
   }
   if (k) {
     const fcg_model_desc& d = lib->desc;
@@ -466,12 +483,6 @@ fcg_status fcg_lib_host_reserve(fcg_lib* lib, int64_t host_tokens) {
       if (lib->host_k) hipHostFree(lib->host_k);
       lib->host_k = nullptr;
       return fail(FCG_ENOMEM, "pinned host slabs");
-    }
-    if (hipEventCreateWithFlags(&lib->freed, hipEventDisableTiming) != hipSuccess) {
-      hipHostFree(lib->host_k);
-      hipHostFree(lib->host_v);
-      lib->host_k = lib->host_v = nullptr;
-      return fail(FCG_EHIP, "hipEventCreate");
     }
   }
   lib->host_cap = host_tokens;
@@ -538,8 +549,10 @@ fcg_status fcg_lib_reload(fcg_lib* lib, int32_t seg_id, void* stream) {
     HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
     hipStream_t s = (hipStream_t)stream;
     fcg_status st = FCG_OK;
-    if (hipStreamWaitEvent(s, lib->freed, 0) != hipSuccess) st = fail(FCG_EHIP, "hipStreamWaitEvent");
+    if (hipStreamWaitEvent(s, lib->freed, 0) != hipSuccess || hipStreamWaitEvent(s, lib->graft_done, 0) != hipSuccess)
+      st = fail(FCG_EHIP, "hipStreamWaitEvent");
     if (!st) st = copy_segment(lib, sg, false, s);
+    if (!st && hipEventRecord(lib->reload_done, s) != hipSuccess) st = fail(FCG_EHIP, "hipEventRecord");
     if (st) {
       lib->release(off, sg.len);
       sg.tok_off = -1;
@@ -555,6 +568,53 @@ fcg_status fcg_lib_segment_state(const fcg_lib* lib, int32_t seg_id, int32_t* in
   const Segment& sg = lib->segs[seg_id];
   if (in_device) *in_device = sg.tok_off >= 0;
   if (on_host) *on_host = sg.host_off >= 0;
+  return FCG_OK;
+}
+
+fcg_status fcg_lib_update_residency(fcg_lib* lib, const fcg_locality* loc, int64_t budget_bytes, double ppl_threshold,
+                                    void* stream, int32_t* n_offloaded, int32_t* n_reloaded) {
+  if (!lib || !loc) return fail(FCG_EINVAL, "null library or scorer");
+  const int32_t n = (int32_t)lib->segs.size();
+  if (locality_size(loc) != n) return fail(FCG_EINVAL, "the scorer must track one function per library segment");
+  if (!(ppl_threshold >= 0)) return fail(FCG_EINVAL, "the perplexity threshold must be >= 0");
+  const fcg_model_desc& d = lib->desc;
+  const int64_t b_tok = 2LL * d.n_layers * d.n_kv_heads * d.head_dim * (int64_t)esize(d.dtype);  // K+V, all layers
+  if (budget_bytes < 0) {
+    // the hyperparameter table's GPU memory threshold and reserve: 0.85 of the
+    // device memory, less 2 GB, less what the rest of the process holds; never
+    // more than the slabs
+    budget_bytes = lib->cap * b_tok;
+    if (!(lib->flags & FCG_LAYOUT_ONLY)) {
+      HIP_TRY(hipSetDevice(lib->device), "hipSetDevice");
+      size_t free_b = 0, total_b = 0;
+      HIP_TRY(hipMemGetInfo(&free_b, &total_b), "hipMemGetInfo");
+      const int64_t others = (int64_t)(total_b - free_b) - lib->cap * b_tok;
+      const int64_t limit = (int64_t)(0.85 * (double)total_b) - (2LL << 30) - std::max<int64_t>(others, 0);
+      budget_bytes = std::max<int64_t>(0, std::min(budget_bytes, limit));
+    }
+  }
+  std::vector<int64_t> cost(n);
+  std::vector<uint8_t> pinned(n), keep(n);
+  for (int32_t f = 0; f < n; ++f) {
+    cost[f] = lib->segs[f].len * b_tok;
+    pinned[f] = lib->segs[f].pins > 0;
+  }
+  if (fcg_status st = locality_residency(loc, budget_bytes, cost.data(), ppl_threshold, pinned.data(), keep.data()))
+    return st;
+  int32_t n_off = 0, n_re = 0;
+  // offloads first: they free the ranges the reloads may take
+  for (int32_t f = 0; f < n; ++f)
+    if (!keep[f] && lib->segs[f].tok_off >= 0) {
+      if (fcg_status st = fcg_lib_offload(lib, f, stream)) return st;
+      ++n_off;
+    }
+  for (int32_t f = 0; f < n; ++f)
+    if (keep[f] && lib->segs[f].tok_off < 0) {
+      if (fcg_status st = fcg_lib_reload(lib, f, stream)) return st;
+      ++n_re;
+    }
+  if (n_offloaded) *n_offloaded = n_off;
+  if (n_reloaded) *n_reloaded = n_re;
   return FCG_OK;
 }
 
@@ -592,6 +652,8 @@ fcg_status fcg_lib_destroy(fcg_lib* lib) {
   if (lib->host_k) hipHostFree(lib->host_k);
   if (lib->host_v) hipHostFree(lib->host_v);
   if (lib->freed) hipEventDestroy(lib->freed);
+  if (lib->graft_done) hipEventDestroy(lib->graft_done);
+  if (lib->reload_done) hipEventDestroy(lib->reload_done);
   delete lib;
   return FCG_OK;
 }
@@ -832,12 +894,15 @@ fcg_status fcg_graft(fcg_cache* c, const fcg_lib* lib, int32_t n_items, const in
   char* dev;
   size_t off;
   if (fcg_status st = upload(c, blob, rows, s, &dev, &off)) return st;
+  if (!(lib->flags & FCG_LAYOUT_ONLY))  // segments reloaded on another stream are in place first
+    HIP_TRY(hipStreamWaitEvent(s, lib->reload_done, 0), "hipStreamWaitEvent");
   const KTime tg{timing_event(c), timing_event(c)};
   int rc = launch_graft(c->desc.dtype, (const GraftChunk*)(dev + o_chunks), (int)chunks.size(), lib->k, lib->v,
                         lib->cap, c->view(), c->d_inv_freq, c->desc.n_layers, s, tg);
   time_open(c, FCG_TIME_GRAFT, tg.start);
   time_close(c, FCG_TIME_GRAFT, tg.stop);
   if (rc) return hip_fail((hipError_t)rc, "graft launch");
+  if (!(lib->flags & FCG_LAYOUT_ONLY)) HIP_TRY(hipEventRecord(lib->graft_done, s), "hipEventRecord");
   if (fcg_status st = c->ring.retire(off, blob.bytes.size(), s)) return st;
   for (auto& sp : spans) c->plan.mark_all_layers(sp.seq, sp.dst, sp.len);
   return FCG_OK;

@@ -20,6 +20,7 @@
 #include <vector>
 
 #include "errors.hpp"
+#include "locality.hpp"
 
 struct fcg_locality {
   int32_t n, window;
@@ -59,6 +60,43 @@ void compute_scores(const fcg_locality& L, double* out) {
 }
 
 }  // namespace
+
+// Residency under a budget (the update step of Alg. 1): entries that must stay
+// (pinned) first, their cost counted; then, in descending score (ties:
+// ascending id), an entry is kept when its cost still fits.  With tau > 0 the
+// entries whose perplexity is below tau come after all the others (the
+// perplexity-based eviction threshold of the hyperparameter table: code the
+// model already predicts well leaves the device tier first).
+fcg_status fcg::locality_residency(const fcg_locality* L, int64_t budget, const int64_t* cost, double tau,
+                                   const uint8_t* pinned, uint8_t* resident) {
+  if (!L || !cost || !resident) return fcg::report(FCG_EINVAL, "null argument");
+  if (budget < 0) return fcg::report(FCG_EINVAL, "negative budget");
+  if (!(tau >= 0)) return fcg::report(FCG_EINVAL, "the perplexity threshold must be >= 0");
+  for (int32_t f = 0; f < L->n; ++f)
+    if (cost[f] < 0) return fcg::report(FCG_EINVAL, "negative cost");
+  std::vector<double> s(L->n);
+  compute_scores(*L, s.data());
+  std::vector<int32_t> order(L->n);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return s[a] > s[b]; });
+  int64_t used = 0;
+  for (int32_t f = 0; f < L->n; ++f) {
+    resident[f] = pinned && pinned[f];
+    if (resident[f]) used += cost[f];
+  }
+  for (int pass = 0; pass < (tau > 0 ? 2 : 1); ++pass)
+    for (int32_t f : order) {
+      if (resident[f]) continue;
+      if (tau > 0 && (L->ppl[f] >= tau) != (pass == 0)) continue;
+      if (used + cost[f] <= budget) {
+        resident[f] = 1;
+        used += cost[f];
+      }
+    }
+  return FCG_OK;
+}
+
+int32_t fcg::locality_size(const fcg_locality* L) { return L ? L->n : 0; }
 
 extern "C" {
 
@@ -100,21 +138,7 @@ fcg_status fcg_locality_scores(const fcg_locality* L, double* scores) {
 }
 
 fcg_status fcg_locality_residency(const fcg_locality* L, int64_t budget, const int64_t* cost, uint8_t* resident) {
-  if (!L || !cost || !resident) return fcg::report(FCG_EINVAL, "null argument");
-  if (budget < 0) return fcg::report(FCG_EINVAL, "negative budget");
-  for (int32_t f = 0; f < L->n; ++f)
-    if (cost[f] < 0) return fcg::report(FCG_EINVAL, "negative cost");
-  std::vector<double> s(L->n);
-  compute_scores(*L, s.data());
-  std::vector<int32_t> order(L->n);
-  std::iota(order.begin(), order.end(), 0);
-  std::stable_sort(order.begin(), order.end(), [&](int32_t a, int32_t b) { return s[a] > s[b]; });
-  int64_t used = 0;
-  for (int32_t f : order) {
-    resident[f] = used + cost[f] <= budget;
-    if (resident[f]) used += cost[f];
-  }
-  return FCG_OK;
+  return fcg::locality_residency(L, budget, cost, 0.0, nullptr, resident);
 }
 
 fcg_status fcg_locality_destroy(fcg_locality* L) {

@@ -33,7 +33,7 @@ FCG_OK, FCG_EINVAL, FCG_ERANGE, FCG_EOVERLAP, FCG_EHOLE, FCG_ENOMEM, FCG_ESTATE,
 # every symbol include/fcg.h declares
 EXPORTS = [
     "fcg_lib_create", "fcg_lib_add_segment", "fcg_lib_segment_info", "fcg_lib_device_ptrs", "fcg_lib_destroy",
-    "fcg_lib_host_reserve", "fcg_lib_offload", "fcg_lib_reload", "fcg_lib_segment_state",
+    "fcg_lib_host_reserve", "fcg_lib_offload", "fcg_lib_reload", "fcg_lib_segment_state", "fcg_lib_update_residency",
     "fcg_cache_create", "fcg_cache_reset", "fcg_cache_truncate", "fcg_cache_export_layout", "fcg_cache_export_v_alias",
     "fcg_cache_device_ptrs",
     "fcg_cache_destroy", "fcg_graft", "fcg_patch_prefill", "fcg_decode", "fcg_decode_noalloc", "fcg_status_string",
@@ -78,6 +78,7 @@ def _load():
         "fcg_lib_offload": [P, I32, P],
         "fcg_lib_reload": [P, I32, P],
         "fcg_lib_segment_state": [P, I32, PI32, PI32],
+        "fcg_lib_update_residency": [P, P, I64, C.c_double, P, PI32, PI32],
         "fcg_cache_create": [C.POINTER(ModelDesc), I32, I32, I32, I32, U32, C.POINTER(P)],
         "fcg_cache_reset": [P, I32],
         "fcg_cache_truncate": [P, I32, I32, P],
@@ -240,6 +241,15 @@ def fcg_lib_segment_state(lib: Library, seg: int):
     a, b = C.c_int32(), C.c_int32()
     _check(_L.fcg_lib_segment_state(lib.h, int(seg), C.byref(a), C.byref(b)))
     return bool(a.value), bool(b.value)
+
+
+def fcg_lib_update_residency(lib: Library, loc: "Locality", budget_bytes: int = -1, ppl_threshold: float = 0.0,
+                             stream=None):
+    """The update step: offload / reload segments by locality under a byte budget -> (offloaded, reloaded)."""
+    a, b = C.c_int32(), C.c_int32()
+    _check(_L.fcg_lib_update_residency(lib.h, loc.h, int(budget_bytes), float(ppl_threshold),
+                                       _stream(stream), C.byref(a), C.byref(b)))
+    return a.value, b.value
 
 
 def fcg_cache_create(desc: ModelDesc, n_seqs: int, max_tokens: int, page_size: int = 0, n_pages: int = 0,

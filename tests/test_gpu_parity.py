@@ -550,3 +550,58 @@ def test_random_small_plans(i):
     copied or read from the library; every sequence checked against the oracle."""
     w, n_dec, alias = _random_case(i)
     run_pipeline(w, [0], n_dec, list(range(w.n_seqs)), alias=alias)
+
+
+@pytest.mark.gpu
+def test_residency_updates_on_a_side_stream_keep_grafts_exact():
+    """The cache-management loop under a tight device budget (Alg. 1: update after each
+    task; Sec. 4.1 and App. C.5: low-scored entries to DRAM, reloaded only when needed):
+    after every task the locality update offloads and reloads segments on a side stream,
+    the next task reloads the segments it needs there too, and its graft on the main
+    stream -- ordered after those copies by the library's events -- equals the oracle's
+    graft of the generated library values (keys within the key bar, values bit for bit),
+    though the segments now sit at other device offsets."""
+    from paper_2606_13097_amd import fcg, runner
+    w = synth.workload("7b", seed=5, n_layers=2, n_lib=16)
+    sh = w.shape
+    b_tok = sh.token_bytes
+    tasks = [synth.workload("7b", seed=5, n_layers=2, n_lib=16, task=t) for t in range(6)]
+    w.max_tokens = max(t.max_tokens for t in tasks)
+    setup = runner.GpuSetup(w, lib_spare_tokens=int(w.lib_lengths.sum()) // 2)
+    side = torch.cuda.Stream()
+    loc = fcg.Locality(len(w.lib_lengths))
+    rng = np.random.default_rng(5)
+    try:
+        lib = setup.lib
+        fcg.fcg_lib_host_reserve(lib, int(w.lib_lengths.sum()))
+        for f in range(len(w.lib_lengths)):
+            fcg.fcg_locality_set_ppl(loc, f, float(rng.uniform(2.0, 30.0)))
+        budget = int(w.lib_lengths.sum() * b_tok * 0.45)
+        winv = rope.inv_freq(sh.head_dim, sh.rope_theta)
+        moves = [0, 0, 0]
+        for t, tw in enumerate(tasks):
+            need = [int(g) for g in tw.graft_seg]
+            for g in need:
+                if not fcg.fcg_lib_segment_state(lib, g)[0]:
+                    fcg.fcg_lib_reload(lib, g, side)
+                    moves[2] += 1
+            setup.reset()
+            fcg.fcg_graft(setup.cache, lib, tw.graft_seq, tw.graft_seg, tw.graft_dst)
+            # the update step right away, on the side stream, beside the graft
+            fcg.fcg_locality_record(loc, need)
+            n_off, n_re = fcg.fcg_lib_update_residency(lib, loc, budget, 15.0, side)
+            moves[0] += n_off
+            moves[1] += n_re
+            torch.cuda.synchronize()
+            for layer in range(sh.n_layers):
+                items = oracle_items(tw, 0, layer)
+                K, V, wr = ograft.compose(tw.max_tokens, sh.n_kv_heads, sh.head_dim, items, winv, sh.dtype)
+                pos = np.flatnonzero(wr)
+                gk, gv = read_cache(setup.cache, tw, layer, 0, pos)
+                np.testing.assert_array_equal(numerics.decode(gv, sh.dtype), V[pos])
+                check_keys(gk, K[pos], sh.dtype, f"task {t} layer {layer} keys after residency updates")
+        say(f"[gpu]   offloads {moves[0]}, reloads by the update {moves[1]}, reloads on demand {moves[2]}")
+        assert moves[0] > 0 and moves[1] + moves[2] > 0
+    finally:
+        loc.close()
+        setup.close()
