@@ -72,6 +72,21 @@ __device__ void merge_splits(const DecodeArgs& args, int i, int hk, int slot0, i
                              float* s_buf, float* s_mt, float* s_lt, int* s_flag) {
   constexpr bool BF = sizeof(T) == 2;
   const int t = threadIdx.x;
+  // Ordering of the cross-block merge, stated in the hardware's terms (the
+  // atomics are relaxed: release/acquire at agent scope would write back and
+  // invalidate the whole L2, ~40 us per launch as measured):
+  //  1. every partial store is a device-scope (sc1) store, written through to
+  //     the device coherence point; s_waitcnt vmcnt(0) returns only once this
+  //     wave's stores are acknowledged there, and the barrier makes that hold
+  //     for all four waves before the block's counter add is issued;
+  //  2. the counter adds are atomic read-modify-writes at that same point, so
+  //     the block that reads nsplit - 1 is ordered after every other block's
+  //     add, hence after all their acknowledged stores;
+  //  3. that block's partial loads are device-scope (sc1) buffer loads served
+  //     by the coherence point, issued only after its add returned: they sit
+  //     behind a branch on the returned count and two barriers (workgroup
+  //     fences), which the compiler does not move memory accesses across.
+  // The many-split and split-edge GPU tests exercise exactly this path.
   wait_vm0();        // this wave's partial stores have completed
   __syncthreads();   // ... and every wave's
   if (t == 0) {
