@@ -73,8 +73,9 @@ __device__ void merge_splits(const DecodeArgs& args, int i, int hk, int slot0, i
   constexpr bool BF = sizeof(T) == 2;
   const int t = threadIdx.x;
   // Ordering of the cross-block merge, stated in the hardware's terms (the
-  // atomics are relaxed: release/acquire at agent scope would write back and
-  // invalidate the whole L2, ~40 us per launch as measured):
+  // atomics are relaxed: release/acquire at agent scope writes back and
+  // invalidates the L2 around the add; an earlier merge built on such fences,
+  // with a serial merge loop, took 50 us per launch):
   //  1. every partial store is a device-scope (sc1) store, written through to
   //     the device coherence point; s_waitcnt vmcnt(0) returns only once this
   //     wave's stores are acknowledged there, and the barrier makes that hold
