@@ -557,8 +557,10 @@ def main():
                        "call_us_per_layer": round(p_ms * 1e3 / (K * sh.n_layers), 2),
                        "call_tflops": round(p_flops / (p_ms / 1e3) / 1e12, 3),
                        "event_span_us_per_layer": round(p_kms * 1e3 / (K * sh.n_layers), 2),
-                       "event_span_note": "first dispatch start to last dispatch end of the call's three kernels "
-                                          "(append, attention, combine) in the timing pass, where each dispatch "
+                       "event_span_note": "first dispatch start to last dispatch end of the call's kernels in the "
+                                          "timing pass (attention, which encodes and appends the fresh tokens "
+                                          "itself, then combine; a separate append kernel runs first only when "
+                                          "a sequence's fresh tokens are not one run), where each dispatch "
                                           "carries its own start/stop events (about 1.4 us each on this GPU); "
                                           "call_* figures come from the timed pass without them"},
         "decode": {"gbs": round(decode_attn_gbs, 2), "frac": round(decode_attn_gbs / HBM_PEAK_GBS, 4),

@@ -104,6 +104,27 @@ __device__ __forceinline__ void wait_vm0() {
   asm volatile("" ::: "memory");
 }
 
+// Reductions over the four lanes l, l ^ 16, l ^ 32, l ^ 48 of a wave (one
+// value per 16-lane row), with the gfx950 lane-swap instructions instead of
+// LDS permutes (__shfl_xor goes through ds_bpermute, an LDS round trip each).
+// Called with one register as both operands, v_permlane16_swap hands every
+// lane its own value and that of lane l ^ 16 as its two results (in an order
+// that depends on the row), and v_permlane32_swap the same for lane l ^ 32;
+// the operations below are commutative, so the order does not matter and all
+// four lanes end with the same bits.
+__device__ __forceinline__ float max_rows4(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_rows4(float v) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  const float m = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(m), __float_as_uint(m), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
 // cos and sin of pos * w for the rotary pair with float64 frequency w: the
 // angle is the float64 product and the float64 cos/sin are rounded to fp32.
 __device__ __forceinline__ void rope_cs(double pos, double w, float* c, float* s) {

@@ -181,36 +181,6 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   const int rows = rb.n_rank * g;
   const float qscale = 1.4426950408889634f / sqrtf((float)D);
 
-  // query rows of this lane: one per 16-row tile (rows past the block's last
-  // one load row 0 and are never written)
-  int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
-  uint4 qf[2][KS];
-  // fused: the raw query dims of the lane, encoded after the first tiles are
-  // in flight.  The rotary partner of dims d (d +- D/2) is the lane's own k
-  // step ks ^ (D / 64).
-  uint4 qa[2][FUSED ? KS : 1];
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const int r = 32 * w + 16 * rt + lr;
-    const int rl = r < rows ? r : 0;
-    if constexpr (FUSED) {
-      // the block's tokens are consecutive positions from rmin, consecutive caller indices
-      const int tr = rl / g;
-      rpos[rt] = rb.rmin + tr;
-      rtok[rt] = rb.ftok0 + (rb.rmin - rb.f0) + tr;
-      const bf16_t* row = raw_q + ((int64_t)rtok[rt] * Hq + hk * g + rl % g) * D;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) qa[rt][ks] = ld16(row + ks * 32 + lq * 8);
-    } else {
-      const TokenMeta m = meta[rb.rank0 + rl / g];
-      rpos[rt] = m.pos;
-      rtok[rt] = m.tok;
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)rb.rank0 * g + rl) * D + ks * 32 + lq * 8);
-    }
-  }
-
   // contiguous caches address a head's rows from one base with 32-bit offsets
   const int64_t head_base = PAGED ? 0 : kv_offset<false>(cv, layer, rb.seq, hk, 0);
   const bf16_t* kbase = ck + head_base;
@@ -266,23 +236,16 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       dma16(src, lds_addr(isv ? B.v : B.k) + jj * 1024);
     }
   };
-  float mrow[2] = {-INFINITY, -INFINITY};
-  float lsum[2] = {0.f, 0.f};
-  floatx4 acc[2][DT];
-#pragma unroll
-  for (int rt = 0; rt < 2; ++rt)
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
-
-  // Prologue: the first kNBuf - 1 tiles go in flight.  The query rows and
-  // metadata were loaded before them; the empty asm makes the compiler wait
-  // for those loads here (it waits for every vector load, these tiles
-  // included), not inside the loop, where its wait would also drain the
-  // prefetched tiles on every pass.
+  // Prologue.  Tile 0 goes in flight first, then the query rows (and the
+  // metadata) are loaded, then the remaining kNBuf - 2 tiles.  The compiler
+  // cannot see the tile loads (inline assembly), so its wait for the query
+  // loads counts none of them and drains every load issued so far: issued in
+  // this order, that wait covers tile 0 only, which step 0 needs anyway,
+  // and leaves the later tiles in flight.
   // fused: the rotary table rows of the block's tokens (consecutive positions,
-  // so one contiguous run of n_rank * D/2 (cos, sin) pairs) go into the ring
-  // buffer that the prologue leaves free, when they fit; else each lane reads
-  // its pairs from the table
+  // so one contiguous run of n_rank * D/2 (cos, sin) pairs) go first, into the
+  // ring buffer that the prologue leaves free, when they fit; else each lane
+  // reads its pairs from the table
   const int cs_bytes = FUSED ? rb.n_rank * HALF * 8 : 0;
   const bool stage_cs = FUSED && cs_bytes <= (int)sizeof(Tile);
   if (FUSED && stage_cs) {
@@ -291,14 +254,42 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     for (int j = wu; j * 64 < nchunk; j += WAVES)
       dma16(src + min(j * 64 + lane, nchunk - 1), lds_addr(&tiles[kNBuf - 1]) + j * 1024);
   }
+  issue_to(0, tiles[0]);  // ntiles >= 1: the split is not empty
+  // query rows of this lane: one per 16-row tile (rows past the block's last
+  // one load row 0 and are never written)
+  int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
+  uint4 qf[2][KS];
+  // fused: the raw query dims of the lane, encoded once they and tile 0 have
+  // landed.  The rotary partner of dims d (d +- D/2) is the lane's own k step
+  // ks ^ (D / 64).
+  uint4 qa[2][FUSED ? KS : 1];
 #pragma unroll
-  for (int i = 0; i < kNBuf - 1; ++i)
-    if (i < ntiles) issue_to(i, tiles[i]);
+  for (int rt = 0; rt < 2; ++rt) {
+    const int r = 32 * w + 16 * rt + lr;
+    const int rl = r < rows ? r : 0;
+    if constexpr (FUSED) {
+      // the block's tokens are consecutive positions from rmin, consecutive caller indices
+      const int tr = rl / g;
+      rpos[rt] = rb.rmin + tr;
+      rtok[rt] = rb.ftok0 + (rb.rmin - rb.f0) + tr;
+      const bf16_t* row = raw_q + ((int64_t)rtok[rt] * Hq + hk * g + rl % g) * D;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qa[rt][ks] = ld16(row + ks * 32 + lq * 8);
+    } else {
+      const TokenMeta m = meta[rb.rank0 + rl / g];
+      rpos[rt] = m.pos;
+      rtok[rt] = m.tok;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks)
+        qf[rt][ks] = ld16(qws + ((int64_t)hk * rows_ws + (int64_t)rb.rank0 * g + rl) * D + ks * 32 + lq * 8);
+    }
+  }
   if constexpr (FUSED) {
     // encode the queries at their positions (rotate-half pairs, fp32 turn,
-    // rounded to bf16), as the append kernel does
+    // rounded to bf16 by the conversion instruction: nearest even, as the
+    // append kernel rounds)
     if (stage_cs) {
-      wait_vm<0>();  // the table rows (issued first) have landed, and this wave's first tiles
+      wait_vm<0>();  // the table rows, tile 0 and the raw queries have landed
       lds_barrier();
     }
     const uint4* cs_lds = reinterpret_cast<const uint4*>(&tiles[kNBuf - 1]);
@@ -325,7 +316,8 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           y[e] = d < HALF ? fmaf(a[e], cs[2 * e], -b[e] * cs[2 * e + 1]) : fmaf(a[e], cs[2 * e], b[e] * cs[2 * e + 1]);
-        qf[rt][ks] = Store<bf16_t>::pack(y);
+        qf[rt][ks] = make_uint4(cvt_bf16x2(y[0], y[1]), cvt_bf16x2(y[2], y[3]), cvt_bf16x2(y[4], y[5]),
+                                cvt_bf16x2(y[6], y[7]));
       }
   }
 #pragma unroll
@@ -334,6 +326,16 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(__builtin_bit_cast(u32x4_t, qf[rt][ks])));
     asm volatile("" ::"v"(rpos[rt]), "v"(rtok[rt]));
   }
+#pragma unroll
+  for (int i = 1; i < kNBuf - 1; ++i)
+    if (i < ntiles) issue_to(i, tiles[i]);
+  float mrow[2] = {-INFINITY, -INFINITY};
+  float lsum[2] = {0.f, 0.f};
+  floatx4 acc[2][DT];
+#pragma unroll
+  for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   // One tile, in ring buffer `buf`: a std::integral_constant on the unrolled
   // path (each step its own instantiation, every LDS address a constant
@@ -382,8 +384,8 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
                 y[e] = c < NC / 2 ? fmaf(a[de], cs[2 * e], -b[de] * cs[2 * e + 1])
                                   : fmaf(a[de], cs[2 * e], b[de] * cs[2 * e + 1]);
               }
-              yw[2 * h] = pack_bf16x2(y[0], y[1]);
-              yw[2 * h + 1] = pack_bf16x2(y[2], y[3]);
+              yw[2 * h] = cvt_bf16x2(y[0], y[1]);
+              yw[2 * h + 1] = cvt_bf16x2(y[2], y[3]);
             }
             asm volatile("" ::: "memory");  // both chunks are read before the write
             const uint4 yk = make_uint4(yw[0], yw[1], yw[2], yw[3]);
@@ -456,8 +458,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
         for (int kt = 0; kt < 4; ++kt)
 #pragma unroll
           for (int e = 0; e < 4; ++e) tmax = fmaxf(tmax, st[rt][kt][e]);
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 16));
-        tmax = fmaxf(tmax, __shfl_xor(tmax, 32));
+        tmax = max_rows4(tmax);
         tmax *= qscale;  // scores are scaled inside the exponent below
         // lazy rescale: the reference max moves only when a row's max grows by
         // more than 2^8 (or on its first visible key); until then
@@ -536,9 +537,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // epilogue: lane holds O^T[d = 16 dt + 4 lq + e][row lr] of each row tile
 #pragma unroll
   for (int rt = 0; rt < 2; ++rt) {
-    float l = lsum[rt];
-    l += __shfl_xor(l, 16);
-    l += __shfl_xor(l, 32);
+    const float l = sum_rows4(lsum[rt]);
     const int r = 32 * w + 16 * rt + lr;
     if (r >= rows) continue;
     if (part < 0) {

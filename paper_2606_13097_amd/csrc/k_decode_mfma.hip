@@ -63,12 +63,18 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   constexpr int HALF = D / 2;
   constexpr int NDG = D / 8;       // 8-dim groups of a row
   constexpr int VBL = 4 * NDG;     // 4-key x 8-dim blocks of a 16-key tile
-  constexpr int VP = 20;           // V^T row pitch in LDS (bf16 elements)
+  // V^T in LDS: row r (a dim, 16 keys = 32 bytes) at element (r + r / 8) * 16,
+  // a 32-byte gap after every 8 rows.  The writes (rows 8 dg + e of one e,
+  // four 8-byte key groups each) and the reads (rows 16 dt .. + 15, all four
+  // groups) then spread over every bank, so that each 512-byte access takes
+  // the minimum number of LDS passes; with plain 32-byte rows the 16 rows of
+  // a write, 8 apart, fall on the same 8 banks.
+  constexpr int VT_ROWS = D + D / 8;
   constexpr int NSL = merge_lanes<bf16_t, D>();
   constexpr int GR = G < 4 ? G : 4;
   constexpr int NBUF = 4 * G * D > GR * NSL * D ? 4 * G * D : GR * NSL * D;
   __shared__ float s_cos[HALF], s_sin[HALF];
-  __shared__ __align__(16) bf16_t s_vt[4][D * VP];
+  __shared__ __align__(16) bf16_t s_vt[4][VT_ROWS * 16];
   __shared__ __align__(16) float s_buf[NBUF];
   __shared__ float s_wm[4][16], s_wl[4][16];
   __shared__ float s_mt[NSL * G], s_lt[NSL * G];
@@ -228,7 +234,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
         const uint32_t sel = (e & 1) ? 0x07060302u : 0x05040100u;
         const uint32_t w01 = __builtin_amdgcn_perm(x[4 + e / 2], x[e / 2], sel);
         const uint32_t w23 = __builtin_amdgcn_perm(x[12 + e / 2], x[8 + e / 2], sel);
-        *reinterpret_cast<uint2*>(&vt[(dg * 8 + e) * VP + kg * 4]) = make_uint2(w01, w23);
+        *reinterpret_cast<uint2*>(&vt[(dg * 9 + e) * 16 + kg * 4]) = make_uint2(w01, w23);  // row 8 dg + e
       }
     }
     dm_f32x4 s = {0.f, 0.f, 0.f, 0.f};
@@ -242,9 +248,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
     }
     if (__builtin_amdgcn_ballot_w64(lmax > mref + 8.f)) {
       // exact running max of each query over its four lanes
-      float mn = fmaxf(mref, lmax);
-      mn = fmaxf(mn, __shfl_xor(mn, 16));
-      mn = fmaxf(mn, __shfl_xor(mn, 32));
+      const float mn = max_rows4(fmaxf(mref, lmax));
       const float f = __builtin_amdgcn_exp2f(mref - mn);  // 0 while nothing was seen
       lsum *= f;
 #pragma unroll
@@ -261,7 +265,8 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
     asm volatile("" ::: "memory");  // the wave's V^T writes come before its reads (LDS is in order per wave)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
-      const uint2 a = *reinterpret_cast<const uint2*>(&vt[(dt * 16 + lr) * VP + 4 * lq]);
+      const int r = dt * 16 + lr;
+      const uint2 a = *reinterpret_cast<const uint2*>(&vt[(r + (r >> 3)) * 16 + 4 * lq]);
       acc[dt] = mma_pv(a, pb, acc[dt]);
     }
     asm volatile("" ::: "memory");  // ... and before the next tile's writes
@@ -294,8 +299,7 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
 
   // ---- merge the four waves: per query, M over the waves, each wave's
   // output and sum weighted by 2^(m - M)
-  lsum += __shfl_xor(lsum, 16);
-  lsum += __shfl_xor(lsum, 32);
+  lsum = sum_rows4(lsum);
   if (lr < G) {
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
