@@ -176,6 +176,11 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
 #pragma unroll
     for (int r = 0; r < 4; ++r) vv[r] = ld16(v_ptr(max(0, min(kb + 4 * kg + r, kend - 1))) + dg * 8);
   };
+  // The loads above go out first: the position's (cos, sin), which the
+  // barrier below waits for, and the query.  Left to itself the scheduler
+  // issues them after the tiles' loads, and that wait then drains the whole
+  // split before the first tile is attended.
+  __builtin_amdgcn_sched_barrier(0);
   uint4 kA[KS], vA[4], kB[KS], vB[4], kC[KS], vC[4];
   load_tile(w, kA, vA);
   load_tile(w + 4, kB, vB);
