@@ -149,6 +149,7 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
     }
   }
   uint4 kr0[U][NV], vr0[U][NV], kr1[U][NV], vr1[U][NV];
+  __builtin_amdgcn_sched_barrier(0);  // the scheduler keeps that order (else the chunks go first)
   load_chunk(k0, kr0, vr0);
   load_chunk(k0 + CK, kr1, vr1);
   if (t < HALF) {
