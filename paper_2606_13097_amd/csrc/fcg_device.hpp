@@ -125,6 +125,36 @@ __device__ __forceinline__ float sum_rows4(float v) {
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
+// Reductions over each 32-lane half of a wave, every lane ending with the
+// half's result (the same bits in all of them: each step combines symmetric
+// pairs of lanes).  Lanes l ^ 1 and l ^ 2 by DPP quad permutes, then the
+// mirrored lane within 8 and within 16 (DPP row_half_mirror, row_mirror),
+// then lane l ^ 16 by v_permlane16_swap; no LDS round trip.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1, 0, 3, 2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141; // lane 7 - l within 8
+constexpr int kDppMirror = 0x140;     // lane 15 - l within 16
+__device__ __forceinline__ float max_lanes32(float v) {
+  v = fmaxf(v, dpp_f32<kDppXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppMirror>(v));
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+}
+__device__ __forceinline__ float sum_lanes32(float v) {
+  v += dpp_f32<kDppXor1>(v);
+  v += dpp_f32<kDppXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(a[0]) + __uint_as_float(a[1]);
+}
+
 // cos and sin of pos * w for the rotary pair with float64 frequency w: the
 // angle is the float64 product and the float64 cos/sin are rounded to fp32.
 __device__ __forceinline__ void rope_cs(double pos, double w, float* c, float* s) {

@@ -227,15 +227,13 @@ __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const To
     if (r < nr) {
       float M = -INFINITY;
       for (int s = l32; s < np; s += 32) M = fmaxf(M, s_f[r][s]);
-#pragma unroll
-      for (int o = 16; o >= 1; o >>= 1) M = fmaxf(M, __shfl_xor(M, o, 32));
+      M = max_lanes32(M);
       float L = 0.f;
       for (int s = l32; s < np; s += 32) {
         const float ms = s_f[r][s];
         L = fmaf(s_l[r][s], ms == -INFINITY ? 0.f : exp2f(ms - M), L);
       }
-#pragma unroll
-      for (int o = 16; o >= 1; o >>= 1) L += __shfl_xor(L, o, 32);
+      L = sum_lanes32(L);
       const float inv = L > 0.f ? 1.f / L : 0.f;
       for (int s = l32; s < np; s += 32) {
         const float ms = s_f[r][s];
