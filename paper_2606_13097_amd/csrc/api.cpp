@@ -1172,6 +1172,7 @@ fcg_status launch_decode_groups(fcg_cache* c, int32_t layer, int32_t n, const in
       a.split0[i + 1] = a.split0[i] + ns;
       a.max_split = std::max(a.max_split, ns);
     }
+    a.slots = a.split0[a.n];
     const size_t qoff = (size_t)i0 * d.n_q_heads * d.head_dim * es, koff = (size_t)i0 * d.n_kv_heads * d.head_dim * es;
     // timing: one kernel, both intervals
     const hipEvent_t e0 = timing ? timing_event(c) : nullptr, e1 = timing ? timing_event(c) : nullptr;

@@ -66,10 +66,13 @@ __device__ __forceinline__ void emit_pair(int nsplit, int64_t prow, T* out_row, 
 
 // Called by all 256 lanes after their emit_pair calls, when nsplit > 1.
 // LDS: s_buf NBUF floats, s_mt / s_lt [256 / (D / EPL)][G] floats, s_flag.
+// Always inlined: called out of line (a choice the compiler made once more
+// kernel instances called it) it made every decode launch ~2 us longer.
 template <typename T, int D, int G, int NBUF>
-__device__ void merge_splits(const DecodeArgs& args, int i, int hk, int slot0, int nsplit, int Hkv, int Hq,
-                             T* __restrict__ out, const float* part_o, const float* part_ml, int* count,
-                             float* s_buf, float* s_mt, float* s_lt, int* s_flag) {
+__device__ __forceinline__ void merge_splits(const DecodeArgs& args, int i, int hk, int slot0, int nsplit, int Hkv,
+                                             int Hq, T* __restrict__ out, const float* part_o,
+                                             const float* part_ml, int* count, float* s_buf, float* s_mt,
+                                             float* s_lt, int* s_flag) {
   constexpr bool BF = sizeof(T) == 2;
   const int t = threadIdx.x;
   // Ordering of the cross-block merge, stated in the hardware's terms (the
@@ -117,7 +120,7 @@ __device__ void merge_splits(const DecodeArgs& args, int i, int hk, int slot0, i
   const int dc = t % NDC, sl = t / NDC;
   const int64_t hg = (int64_t)Hkv * G;          // rows per partial slot
   const int64_t row0 = (int64_t)slot0 * hg + (int64_t)hk * G;
-  const uint32_t rows_all = (uint32_t)(args.split0[args.n] * hg);
+  const uint32_t rows_all = (uint32_t)(args.slots * hg);
   const __amdgpu_buffer_rsrc_t ro = buf_rsrc(part_o, rows_all * D * EB);
   const __amdgpu_buffer_rsrc_t rml = buf_rsrc(part_ml, rows_all * 8u);
   float acc[G][EPL], lm[G], ll[G];

@@ -135,32 +135,40 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // causal mask leaves to fewer row blocks, spread over the XCDs).  Ids past
   // the last group exit.
   const int Hkv = cv.n_kv_heads;
-  int rbi, split, hk;
+  // Every kernel argument the block reads is fetched in one batch of scalar
+  // loads before the first branch: left to the compiler, the loads are placed
+  // next to their uses, and a load whose address depends on a loaded value
+  // (the row block, indexed by an id that depends on the launch's order) waits
+  // for a round trip of its own.  So both candidate row blocks are fetched
+  // (indices from the block id alone, clamped into the array) and one is
+  // chosen once the batch has landed.
+  const PrefillRb rb_plain = args.rb[min((int)blockIdx.x, kPfMaxRb - 1)];
+  const PrefillRb rb_xcd = args.rb[blockIdx.x / kXcds];
+  const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
+  const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
+  asm volatile("" ::"s"(rb_plain.rank0), "s"(rb_plain.n_rank), "s"(rb_plain.seq), "s"(rb_plain.rmin), "s"(rb_plain.pmax),
+               "s"(rb_plain.part0), "s"(rb_xcd.rank0), "s"(rb_xcd.n_rank), "s"(rb_xcd.seq), "s"(rb_xcd.rmin),
+               "s"(rb_xcd.pmax), "s"(rb_xcd.part0), "s"(args.n_rb), "s"(args.n_split), "s"(args.span), "s"(args.xcd_group));
+  asm volatile("" ::"s"(meta), "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens),
+               "s"(Hkv), "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
+  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
+  if (FUSED)
+    asm volatile("" ::"s"(rb_plain.f0), "s"(rb_plain.ftok0), "s"(rb_xcd.f0), "s"(rb_xcd.ftok0), "s"(raw_q), "s"(raw_k),
+                 "s"(raw_v), "s"(rope));
+  __builtin_amdgcn_sched_barrier(0);
+  int split, hk;
   if (args.xcd_group) {
-    const int xcd = blockIdx.x % kXcds;
-    rbi = blockIdx.x / kXcds;
-    const int grp = blockIdx.y * kXcds + xcd;
+    const int grp = blockIdx.y * kXcds + blockIdx.x % kXcds;
     split = grp / Hkv;
     hk = grp % Hkv;
   } else {
-    rbi = blockIdx.x;
     split = blockIdx.y;
     hk = blockIdx.z;
   }
-  const PrefillRb rb = args.rb[rbi];
+  const PrefillRb rb = args.xcd_group ? rb_xcd : rb_plain;
   const int k0 = split * args.span;
   const int kend = min(rb.pmax + 1, k0 + args.span);
   const int part = rb.part0 < 0 ? -1 : rb.part0 + split;
-  const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
-  const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
-  // Every kernel argument the block reads, fetched in one batch of scalar
-  // loads before the first branch: left to the compiler, the loads are placed
-  // next to their uses and each costs a memory round trip of its own.
-  asm volatile("" ::"s"(rb.rank0), "s"(rb.n_rank), "s"(rb.seq), "s"(rb.rmin), "s"(kend), "s"(part), "s"(meta),
-               "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(Hkv),
-               "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
-  if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
-  if (FUSED) asm volatile("" ::"s"(rb.f0), "s"(rb.ftok0), "s"(rb.pmax), "s"(raw_q), "s"(raw_k), "s"(raw_v), "s"(rope));
   if (split >= args.n_split || k0 >= kend) return;  // past the last group; padding split of a shorter row block
   const int g = Hq / Hkv;
   const int t = threadIdx.x;

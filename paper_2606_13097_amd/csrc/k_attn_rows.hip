@@ -178,13 +178,16 @@ __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const To
   __shared__ float4 s_acc[256];
   const CombineItem it = args.item[blockIdx.x];
   const int hk = blockIdx.y;
+  // every argument in one batch of scalar loads, before any arithmetic on
+  // them (else the compiler issues part of the batch after the division)
+  asm volatile("" ::"s"(it.rank0), "s"(it.n_rank), "s"(it.n_part), "s"(it.part0), "s"(it.tok0), "s"(meta), "s"(part_o),
+               "s"(part_ml), "s"(out), "s"(Hq), "s"(Hkv), "s"(part_stride_rows));
+  __builtin_amdgcn_sched_barrier(0);
   const int g = Hq / Hkv;
   const int t = threadIdx.x;
   const int r0 = blockIdx.z * kCombRows;
   const int nr = min(kCombRows, it.n_rank * g - r0);
   const int np = it.n_part;
-  asm volatile("" ::"s"(it.rank0), "s"(nr), "s"(np), "s"(it.part0), "s"(it.tok0), "s"(meta), "s"(part_o), "s"(part_ml),
-               "s"(out), "s"(Hq), "s"(Hkv), "s"(part_stride_rows));
   if (nr <= 0) return;
   auto prow = [&](int s, int r) { return ((int64_t)(it.part0 + s) * Hkv + hk) * part_stride_rows + r0 + r; };
   constexpr int CPR = D / 4;                  // 4-dim chunks per row

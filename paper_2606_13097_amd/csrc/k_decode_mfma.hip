@@ -350,15 +350,13 @@ int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, con
   if (args.n == 0) return 0;
   const int g = Hq / cv.n_kv_heads;
   dim3 grid(args.max_split, args.n, cv.n_kv_heads);
+#define DM1(DD, GG, PG)                                                                                       \
+  hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, PG>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args,   \
+                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out,   \
+                        part_o, part_ml, count)
 #define DM(DD, GG)                                                                                            \
-  if (cv.page_size)                                                                                           \
-    hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, \
-                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out, \
-                          part_o, part_ml, count);                                                            \
-  else                                                                                                        \
-    hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, \
-                          (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out, \
-                          part_o, part_ml, count)
+  if (cv.page_size) DM1(DD, GG, true);                                                                        \
+  else DM1(DD, GG, false)
 #define DMG(DD)                                                                                               \
   switch (g) {                                                                                                \
     case 1: DM(DD, 1); break;                                                                                 \
@@ -371,6 +369,7 @@ int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, con
   if (cv.head_dim == 64) { DMG(64) } else { DMG(128) }
 #undef DMG
 #undef DM
+#undef DM1
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? 0 : (int)e;
 }

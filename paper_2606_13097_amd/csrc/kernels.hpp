@@ -117,7 +117,7 @@ struct DecodeArgs {
   int32_t n;           // sequences in this launch
   int32_t split_keys;  // key positions per split
   int32_t max_split;   // largest split count of the launch (grid x)
-  int32_t pad;
+  int32_t slots;       // partial slots of the launch, split0[n] (a field of its own, at a fixed offset)
   int32_t seq[kMaxDecodeSeqs];
   int32_t pos[kMaxDecodeSeqs];         // the new token's position (= the sequence's length)
   int32_t split0[kMaxDecodeSeqs + 1];  // first partial slot of each sequence; split0[i + 1] - split0[i] splits
