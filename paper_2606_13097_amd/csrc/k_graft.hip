@@ -39,9 +39,10 @@ __global__ void __launch_bounds__(256) ingest_kernel(const T* __restrict__ k, co
 
 // Library reads and cache writes of the graft.  Contiguous caches: reads with
 // the nontemporal hint (read once), plain stores (the cache is read next).  Paged
-// caches, whose runs land in 4 KB page pieces: plain reads and nontemporal
-// stores (batched workload: 10.2 -> 9.6 ms per graft; the same choice on a
-// contiguous cache was slower).
+// caches, whose runs land in 4 KB page pieces: plain reads, so that segments
+// several tasks of a batch share are served from cache, and nontemporal stores
+// (batched workload: 10.2 -> 6.7 ms per graft; the same choice on a contiguous
+// cache was slower).
 template <bool PAGED>
 __device__ __forceinline__ uint4 ld_lib(const void* p) {
   return PAGED ? ld16(p) : ld16_nt(p);
