@@ -326,13 +326,16 @@ void time_drop(fcg_cache* c, hipEvent_t e) {
 
 fcg_status grow(void** p, size_t* have, size_t need, const char* what) {
   if (need <= *have) return FCG_OK;
+  // at least twice the old size, so that a workload whose need creeps up (a
+  // sequence crossing a split boundary every few decode steps) reallocates
+  // rarely: each reallocation waits for the device
+  const size_t n = std::max(need, *have * 2);
   if (*p) {
     HIP_TRY(hipDeviceSynchronize(), "hipDeviceSynchronize(grow)");
     hipFree(*p);
     *p = nullptr;
     *have = 0;
   }
-  size_t n = std::max(need, *have * 2);
   hipError_t e = hipMalloc(p, n);
   if (e != hipSuccess) return fail(FCG_ENOMEM, std::string("hipMalloc(") + what + ") failed");
   *have = n;
