@@ -146,9 +146,10 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   const PrefillRb rb_xcd = args.rb[blockIdx.x / kXcds];
   const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
   const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
-  asm volatile("" ::"s"(rb_plain.rank0), "s"(rb_plain.n_rank), "s"(rb_plain.seq), "s"(rb_plain.rmin), "s"(rb_plain.pmax),
-               "s"(rb_plain.part0), "s"(rb_xcd.rank0), "s"(rb_xcd.n_rank), "s"(rb_xcd.seq), "s"(rb_xcd.rmin),
-               "s"(rb_xcd.pmax), "s"(rb_xcd.part0), "s"(args.n_rb), "s"(args.n_split), "s"(args.span), "s"(args.xcd_group));
+  asm volatile("" ::"s"(rb_plain.rank0), "s"(rb_plain.n_rank), "s"(rb_plain.seq), "s"(rb_plain.rmin),
+               "s"(rb_plain.pmax), "s"(rb_plain.part0), "s"(rb_xcd.rank0), "s"(rb_xcd.n_rank), "s"(rb_xcd.seq),
+               "s"(rb_xcd.rmin), "s"(rb_xcd.pmax), "s"(rb_xcd.part0), "s"(args.n_rb), "s"(args.n_split),
+               "s"(args.span), "s"(args.xcd_group));
   asm volatile("" ::"s"(meta), "s"(qws), "s"(rows_ws), "s"(ck), "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens),
                "s"(Hkv), "s"(layer), "s"(Hq), "s"(out), "s"(part_o), "s"(part_ml), "s"(part_stride_rows));
   if (PAGED) asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap));
