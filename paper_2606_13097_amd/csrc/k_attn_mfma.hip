@@ -166,7 +166,18 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     split = blockIdx.y;
     hk = blockIdx.z;
   }
-  const PrefillRb rb = args.xcd_group ? rb_xcd : rb_plain;
+  // chosen field by field: a select of the whole struct was lowered to a copy
+  // of both candidates into scratch memory and a load at a computed offset
+  const bool xg = args.xcd_group != 0;
+  PrefillRb rb;
+  rb.rank0 = xg ? rb_xcd.rank0 : rb_plain.rank0;
+  rb.n_rank = xg ? rb_xcd.n_rank : rb_plain.n_rank;
+  rb.seq = xg ? rb_xcd.seq : rb_plain.seq;
+  rb.rmin = xg ? rb_xcd.rmin : rb_plain.rmin;
+  rb.pmax = xg ? rb_xcd.pmax : rb_plain.pmax;
+  rb.part0 = xg ? rb_xcd.part0 : rb_plain.part0;
+  rb.f0 = xg ? rb_xcd.f0 : rb_plain.f0;
+  rb.ftok0 = xg ? rb_xcd.ftok0 : rb_plain.ftok0;
   const int k0 = split * args.span;
   const int kend = min(rb.pmax + 1, k0 + args.span);
   const int part = rb.part0 < 0 ? -1 : rb.part0 + split;

@@ -62,9 +62,9 @@ __device__ __forceinline__ float lanes_sum_stride(float x) {
 template <typename T, int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* __restrict__ q,
                                                      const T* __restrict__ k, const T* __restrict__ v, CacheView cv,
-                                                     int layer, const float2* __restrict__ rope,
-                                                     T* __restrict__ out, float* __restrict__ part_o,
-                                                     float* __restrict__ part_ml, int* __restrict__ count) {
+                                                     const float2* __restrict__ rope, T* __restrict__ out,
+                                                     float* __restrict__ part_o, float* __restrict__ part_ml,
+                                                     int* __restrict__ count, int layer) {
   constexpr int VEC = Store<T>::VEC;
   constexpr int NV = (D / VEC > 16) ? (D / VEC) / 16 : 1;
   constexpr int DPL = VEC * NV;    // dims per lane
@@ -92,10 +92,14 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs args, const T* _
   const int sk = args.split_keys;
   const T* ck = reinterpret_cast<const T*>(cv.k);
   const T* cvv = reinterpret_cast<const T*>(cv.v);
-  // every kernel argument in one batch of scalar loads before the first branch
+  // every kernel argument in one batch of scalar loads before the first branch.
+  // The batch must not load a dword nothing reads: the compiler may reuse its
+  // register for a later load of the batch, which then waits for the first
+  // loads to land (a second round trip).  So `layer` comes last (no padding
+  // after it) and the unused head_dim, which a merged load covers, is listed.
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
                "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(rope),
-               "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
+               "s"(out), "s"(part_o), "s"(part_ml), "s"(count), "s"(cv.head_dim));
   if (PAGED)
     asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap), "s"(npage));
   if (split >= nsplit) return;  // padding split of a shorter sequence
@@ -366,10 +370,10 @@ int launch_decode(int dtype, const DecodeArgs& args, const void* q, const void* 
 #define DK(T, DD, GG)                                                                                       \
   if (cv.page_size)                                                                                         \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, true>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,          \
-                       (const T*)k, (const T*)v, cv, layer, rope, (T*)out, part_o, part_ml, count);             \
+                       (const T*)k, (const T*)v, cv, rope, (T*)out, part_o, part_ml, count, layer);             \
   else                                                                                                      \
     hipExtLaunchKernelGGL((decode_kernel<T, DD, GG, false>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args, (const T*)q,         \
-                       (const T*)k, (const T*)v, cv, layer, rope, (T*)out, part_o, part_ml, count)
+                       (const T*)k, (const T*)v, cv, rope, (T*)out, part_o, part_ml, count, layer)
 #define DKG(T, DD)                                                                                          \
   switch (g) {                                                                                              \
     case 1: DK(T, DD, 1); break;                                                                            \

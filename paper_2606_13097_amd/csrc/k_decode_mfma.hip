@@ -53,10 +53,11 @@ __device__ __forceinline__ uint32_t dm_cvt_bf16x2(float lo, float hi) {
 template <int D, int G, bool PAGED>
 __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const bf16_t* __restrict__ q,
                                                           const bf16_t* __restrict__ k,
-                                                          const bf16_t* __restrict__ v, CacheView cv, int layer,
+                                                          const bf16_t* __restrict__ v, CacheView cv,
                                                           const float2* __restrict__ rope,
                                                           bf16_t* __restrict__ out, float* __restrict__ part_o,
-                                                          float* __restrict__ part_ml, int* __restrict__ count) {
+                                                          float* __restrict__ part_ml, int* __restrict__ count,
+                                                          int layer) {
   static_assert(G >= 1 && G <= 16, "query group");
   constexpr int KS = D / 32;       // 32-deep k steps of S^T
   constexpr int DT = D / 16;       // 16-dim tiles of O^T
@@ -92,10 +93,14 @@ __global__ void __launch_bounds__(256) decode_mfma_kernel(DecodeArgs args, const
   const int sk = args.split_keys;
   const bf16_t* ck = reinterpret_cast<const bf16_t*>(cv.k);
   const bf16_t* cvv = reinterpret_cast<const bf16_t*>(cv.v);
-  // every kernel argument in one batch of scalar loads before the first branch
+  // every kernel argument in one batch of scalar loads before the first branch.
+  // The batch must not load a dword nothing reads: the compiler may reuse its
+  // register for a later load of the batch, which then waits for the first
+  // loads to land (a second round trip).  So `layer` comes last (no padding
+  // after it) and the unused head_dim, which a merged load covers, is listed.
   asm volatile("" ::"s"(seq), "s"(pos), "s"(slot0), "s"(nsplit), "s"(sk), "s"(q), "s"(k), "s"(v), "s"(ck),
                "s"(cvv), "s"(cv.layer_stride), "s"(cv.max_tokens), "s"(cv.n_kv_heads), "s"(layer), "s"(rope),
-               "s"(out), "s"(part_o), "s"(part_ml), "s"(count));
+               "s"(out), "s"(part_o), "s"(part_ml), "s"(count), "s"(cv.head_dim));
   if (PAGED)
     asm volatile("" ::"s"(cv.page_table), "s"(cv.n_lp), "s"(cv.v_alias), "s"(cv.lib_v), "s"(cv.lib_cap), "s"(npage));
   if (split >= nsplit) return;  // padding split of a shorter sequence
@@ -352,8 +357,8 @@ int launch_decode_mfma(const DecodeArgs& args, const void* q, const void* k, con
   dim3 grid(args.max_split, args.n, cv.n_kv_heads);
 #define DM1(DD, GG, PG)                                                                                       \
   hipExtLaunchKernelGGL((decode_mfma_kernel<DD, GG, PG>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args,   \
-                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, layer, rope, (bf16_t*)out,   \
-                        part_o, part_ml, count)
+                        (const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, cv, rope, (bf16_t*)out, part_o,   \
+                        part_ml, count, layer)
 #define DM(DD, GG)                                                                                            \
   if (cv.page_size) DM1(DD, GG, true);                                                                        \
   else DM1(DD, GG, false)

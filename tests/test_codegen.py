@@ -1,13 +1,21 @@
 """Checks on the gfx950 code objects inside the built ``libfcg.so`` (no GPU needed).
 
-Every device function must be inlined into its kernel: a function called out of
-line needs a call frame and register save/restore on every launch.  The decode
-kernel's split merge once ended up out of line (the compiler's choice when more
-kernel instances called it) and every decode launch took ~2 us longer.  In the
-code objects an out-of-line device function shows as a FUNC symbol without the
-kernel descriptor (``<name>.kd``) that every kernel has.
+- Every device function must be inlined into its kernel: a function called out
+  of line needs a call frame and register save/restore on every launch.  The
+  decode kernel's split merge once ended up out of line (the compiler's choice
+  when more kernel instances called it) and every decode launch took ~2 us
+  longer.  In the code objects an out-of-line device function shows as a FUNC
+  symbol without the kernel descriptor (``<name>.kd``) that every kernel has.
+- The attention kernels fetch their arguments in one batch of scalar loads: one
+  wait for them before the first branch.  A second batch costs a memory round
+  trip at the start of every launch; it appears when a merged load covers a
+  dword that nothing reads and the compiler reuses that register.
+- The hot kernels use no scratch memory.  A select between two row-block
+  structs was once lowered to a copy of both into scratch and a load at a
+  computed offset.
 """
 import os
+import re
 import shutil
 import subprocess
 import tempfile
@@ -17,7 +25,7 @@ import pytest
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 LIB = os.path.join(ROOT, "paper_2606_13097_amd", "libfcg.so")
 LLVM = "/opt/rocm/llvm/bin"
-TOOLS = [os.path.join(LLVM, t) for t in ("llvm-objcopy", "clang-offload-bundler", "llvm-readelf")]
+TOOLS = [os.path.join(LLVM, t) for t in ("llvm-objcopy", "clang-offload-bundler", "llvm-readelf", "llvm-objdump")]
 TARGET = "hipv4-amdgcn-amd-amdhsa--gfx950"
 MAGIC = b"__CLANG_OFFLOAD_BUNDLE__"
 
@@ -42,6 +50,32 @@ def _code_objects(tmp):
                        check=True, capture_output=True)
         objs.append(co)
     return objs
+
+
+def _disassembly(co):
+    """{kernel name: its instructions} from the disassembler."""
+    out = subprocess.run([TOOLS[3], "-d", co], check=True, capture_output=True, text=True).stdout
+    kernels, cur = {}, None
+    for line in out.splitlines():
+        m = re.match(r"^[0-9a-f]+ <(\S+)>:", line)
+        if m:
+            cur = kernels.setdefault(m.group(1), [])
+        elif cur is not None and line.strip():
+            cur.append(line.split("//")[0].strip())
+    return kernels
+
+
+def _private_sizes(co):
+    """{kernel name: private segment (scratch) bytes per lane} from the code object's metadata."""
+    out = subprocess.run([TOOLS[2], "--notes", co], check=True, capture_output=True, text=True).stdout
+    sizes, name = {}, None
+    for line in out.splitlines():
+        f = line.split()
+        if len(f) == 2 and f[0] == ".name:":
+            name = f[1]
+        if len(f) == 2 and f[0] == ".private_segment_fixed_size:" and name:
+            sizes[name] = int(f[1])
+    return sizes
 
 
 def _symbols(co):
@@ -70,5 +104,52 @@ def test_every_device_function_is_inlined_into_its_kernel():
             outlined += sorted(f for f in funcs if f not in kds)
         assert kernels > 0
         assert not outlined, f"device functions called out of line: {outlined[:5]}"
+    finally:
+        shutil.rmtree(tmp, ignore_errors=True)
+
+
+ONE_BATCH = ("decode_mfma_kernel", "decode_kernel", "attn_prefill_mfma_kernel", "combine_kernel")
+# Known exceptions, bounded:
+# - the paged, fused, two-blocks-per-CU prefill holds 256 registers: one 8-byte
+#   value lives in scratch from the prologue to the epilogue (outside the tile loop);
+# - the fp32 decode with 16 query heads per kv head and head_dim 128 holds the 16
+#   raw query rows and their rotary partners in registers through the prologue
+#   (no workload here has that shape; bf16 caches take the matrix-core kernel).
+SCRATCH_ALLOWED = {"attn_prefill_mfma_kernelILi128ELb1ELi4ELi2ELb1E": 16, "decode_kernelIfLi128ELi16E": 192}
+NO_SCRATCH = ONE_BATCH + ("graft_kernel", "rope_append_kernel")
+
+
+def _family(name, fams):
+    return next((f for f in fams if f in name), None)
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="libfcg.so is not built")
+@pytest.mark.skipif(not all(os.path.exists(t) for t in TOOLS), reason="ROCm LLVM tools not found")
+def test_attention_kernels_fetch_their_arguments_in_one_batch_and_use_no_scratch():
+    tmp = tempfile.mkdtemp(prefix="fcg_codegen_")
+    try:
+        checked, split, scratch = 0, [], []
+        for co in _code_objects(tmp):
+            for name, ins in _disassembly(co).items():
+                if not _family(name, ONE_BATCH):
+                    continue
+                head = []
+                for i in ins:
+                    if i.startswith(("s_cbranch", "s_branch", "s_endpgm")):
+                        break
+                    head.append(i)
+                waits = sum(1 for i in head if i.startswith("s_waitcnt") and "lgkmcnt(0)" in i)
+                checked += 1
+                if waits != 1:
+                    split.append((name, waits))
+            for name, size in _private_sizes(co).items():
+                if not _family(name, NO_SCRATCH):
+                    continue
+                limit = next((v for k, v in SCRATCH_ALLOWED.items() if k in name), 0)
+                if size > limit:
+                    scratch.append((name, size))
+        assert checked >= 40, checked
+        assert not split, f"argument loads in more than one batch: {split[:4]}"
+        assert not scratch, f"scratch memory in hot kernels: {scratch[:4]}"
     finally:
         shutil.rmtree(tmp, ignore_errors=True)
