@@ -154,31 +154,62 @@ def copy_probe(gib: float) -> None:
 
 
 def copy_ceiling(total_bytes, graft_gbs, reps=10):
-    """A plain device-to-device copy (torch copy_) that reads and writes as many bytes as one
-    graft launch, timed on the same GPU: the practical ceiling for a pure stream."""
+    """Stream ceilings on the same GPU for as many bytes as one graft launch moves:
+    a device-to-device copy through torch (copy_), and the copy, read and write
+    kernels of measure/libfcg_measure.so (the fastest variants of a sweep over block
+    size and cache hints).  Half the bytes are read and half written, as in the graft."""
+    import ctypes as C
     import torch
-    n = total_bytes // 4                     # bf16 elements per buffer: half the bytes each way
-    a = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    n = total_bytes // 4 // 8 * 8            # bf16 elements per buffer: half the bytes each way (16-byte multiple)
+    half = 2 * n
+    a = torch.zeros(n, dtype=torch.bfloat16, device="cuda")
     b = torch.empty_like(a)
-    b.copy_(a)
-    torch.cuda.synchronize()
-    times = []
-    for _ in range(reps):
-        e0 = torch.cuda.Event(enable_timing=True)
-        e1 = torch.cuda.Event(enable_timing=True)
-        e0.record()
-        b.copy_(a)
-        e1.record()
-        e1.synchronize()
-        times.append(e0.elapsed_time(e1))
-    ms = sorted(times)[len(times) // 2]
-    moved = 4 * n                            # read + write
+    lib = C.CDLL(os.path.join(ROOT, "paper_2606_13097_amd", "measure", "libfcg_measure.so"))
+    lib.fcg_measure_stream.argtypes = [C.c_int, C.c_void_p, C.c_void_p, C.c_longlong, C.c_void_p]
+    lib.fcg_measure_stream.restype = C.c_int
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            times.append(e0.elapsed_time(e1))
+        return sorted(times)[len(times) // 2]
+
+    def probe(mode, src, dst):
+        def fn():
+            if lib.fcg_measure_stream(mode, C.c_void_p(src), C.c_void_p(dst), half, C.c_void_p(stream)):
+                raise RuntimeError("fcg_measure_stream failed")
+        return fn
+
+    ms_torch = timed(lambda: b.copy_(a))
+    ms_copy = timed(probe(0, a.data_ptr(), b.data_ptr()))
+    ms_read = timed(probe(1, a.data_ptr(), b.data_ptr()))
+    ms_write = timed(probe(2, 0, b.data_ptr()))
     del a, b
     torch.cuda.empty_cache()
-    gbs = moved / (ms / 1e3) / 1e9
-    return {"kind": "device-to-device copy (torch copy_) of the graft launch's byte count, median of "
-                    f"{reps}", "bytes": moved, "us": round(ms * 1e3, 2), "gbs": round(gbs, 2),
-            "graft_over_copy": round(graft_gbs / gbs, 3)}
+    moved = 2 * half
+    g = lambda nbytes, ms: round(nbytes / (ms / 1e3) / 1e9, 2)
+    gk, gr, gw = g(moved, ms_copy), g(half, ms_read), g(half, ms_write)
+    return {"kind": f"stream kernels over the graft launch's byte count (half read, half written), median of {reps}",
+            "bytes": moved,
+            "torch_copy": {"us": round(ms_torch * 1e3, 2), "gbs": g(moved, ms_torch)},
+            "copy_kernel": {"us": round(ms_copy * 1e3, 2), "gbs": gk},
+            "read_kernel": {"bytes": half, "us": round(ms_read * 1e3, 2), "gbs": gr},
+            "write_kernel": {"bytes": half, "us": round(ms_write * 1e3, 2), "gbs": gw},
+            "read_then_write_gbs": round(2 / (1 / gr + 1 / gw), 2),
+            "gbs": g(moved, ms_torch), "us": round(ms_torch * 1e3, 2),
+            "graft_over_copy": round(graft_gbs / g(moved, ms_torch), 3),
+            "graft_over_copy_kernel": round(graft_gbs / gk, 3),
+            "note": "read_then_write_gbs: the rate if the launch's reads ran at the read kernel's rate and its "
+                    "writes at the write kernel's, one after the other"}
 
 
 def graft_bytes(tw, kvb, n_layers, alias_v):

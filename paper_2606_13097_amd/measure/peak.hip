@@ -1,5 +1,8 @@
-// Matrix-core issue rate of this GPU, for the bench's roofline context (not a
-// step of the grafting path).  Every wave runs `iters` rounds of eight
+// Probes of this GPU's ceilings, for the bench's roofline context (not steps
+// of the grafting path): the matrix-core issue rate, and the HBM stream rates
+// of plain copy, read and write kernels.
+//
+// Matrix-core issue rate.  Every wave runs `iters` rounds of eight
 // independent bf16 v_mfma_f32_16x16x32 chains on register operands: no memory
 // traffic, no dependent stalls (eight chains cover the instruction's
 // latency), so the rate is what the matrix cores sustain at the clock the
@@ -88,5 +91,73 @@ extern "C" int fcg_measure_mfma_rate(int blocks, int iters, float* out, void* st
     hipLaunchKernelGGL(mfma_rate_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters, out);
   else
     hipLaunchKernelGGL(mfma32_rate_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream, iters, out);
+  return (int)hipGetLastError();
+}
+
+// HBM stream rates.  Each block moves V16 x 256 16-byte vectors, issuing every
+// load before any store; the grid covers the buffer once.  The variants are the
+// fastest ones of a sweep over block sizes (4-64 KB) and cache hints on this GPU:
+//   copy:  32 KB per block, nontemporal loads and stores;
+//   read:  64 KB per block, nontemporal loads, folded into one value per lane
+//          (stored only if it matches a pattern zeroed input never gives);
+//   write: 16 KB per block, plain stores.
+typedef unsigned int u32x4_m __attribute__((ext_vector_type(4)));
+
+template <int V16>
+__global__ void __launch_bounds__(256) stream_copy_kernel(const u32x4_m* __restrict__ src, u32x4_m* __restrict__ dst,
+                                                          long long nvec) {
+  const long long base = (long long)blockIdx.x * V16 * 256 + threadIdx.x;
+  u32x4_m r[V16];
+#pragma unroll
+  for (int i = 0; i < V16; ++i) {
+    const long long j = base + i * 256;
+    r[i] = __builtin_nontemporal_load(src + (j < nvec ? j : nvec - 1));
+  }
+#pragma unroll
+  for (int i = 0; i < V16; ++i) {
+    const long long j = base + i * 256;
+    if (j < nvec) __builtin_nontemporal_store(r[i], dst + j);
+  }
+}
+
+template <int V16>
+__global__ void __launch_bounds__(256) stream_read_kernel(const u32x4_m* __restrict__ src, u32x4_m* __restrict__ sink,
+                                                          long long nvec) {
+  const long long base = (long long)blockIdx.x * V16 * 256 + threadIdx.x;
+  u32x4_m a = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int i = 0; i < V16; ++i) {
+    const long long j = base + i * 256;
+    a ^= __builtin_nontemporal_load(src + (j < nvec ? j : nvec - 1));
+  }
+  if (a.x == 0x12345678u && a.y == 0x9abcdef0u) sink[threadIdx.x] = a;
+}
+
+template <int V16>
+__global__ void __launch_bounds__(256) stream_write_kernel(u32x4_m* __restrict__ dst, long long nvec) {
+  const long long base = (long long)blockIdx.x * V16 * 256 + threadIdx.x;
+#pragma unroll
+  for (int i = 0; i < V16; ++i) {
+    const long long j = base + i * 256;
+    if (j < nvec) dst[j] = u32x4_m{(unsigned)j, 1u, 2u, 3u};
+  }
+}
+
+// extern "C" int fcg_measure_stream(int mode, const void* src, void* dst, long long bytes, void* stream)
+//   mode 0: copy bytes from src to dst; 1: read bytes of src (zeroed input;
+//   dst: a sink of at least 4 KB that stays untouched); 2: write bytes to dst
+//   (src unused).  bytes: a positive multiple of 16.  Returns 0, or the HIP error.
+extern "C" int fcg_measure_stream(int mode, const void* src, void* dst, long long bytes, void* stream) {
+  if (mode < 0 || mode > 2 || bytes < 16 || bytes % 16 || !dst || (mode < 2 && !src)) return (int)hipErrorInvalidValue;
+  const long long nvec = bytes / 16;
+  hipStream_t s = (hipStream_t)stream;
+  const u32x4_m* in = (const u32x4_m*)src;
+  u32x4_m* out = (u32x4_m*)dst;
+  if (mode == 0)
+    hipLaunchKernelGGL(stream_copy_kernel<8>, dim3((unsigned)((nvec + 2047) / 2048)), dim3(256), 0, s, in, out, nvec);
+  else if (mode == 1)
+    hipLaunchKernelGGL(stream_read_kernel<16>, dim3((unsigned)((nvec + 4095) / 4096)), dim3(256), 0, s, in, out, nvec);
+  else
+    hipLaunchKernelGGL(stream_write_kernel<4>, dim3((unsigned)((nvec + 1023) / 1024)), dim3(256), 0, s, out, nvec);
   return (int)hipGetLastError();
 }
