@@ -518,18 +518,22 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       // 32 s + 4 lq + lr / 4 (+ 16), dims 16 dt + 4 (lr % 4) .. + 3.
       const int vr = 4 * lq + (lr >> 2);                 // row within a 32-key step
       const int vsw = Tile::swz_v(vr);                   // the same for rows vr + 16, + 32, + 48
+      // fragment i = 2 dt + s; the next fragment's reads go out before the
+      // current fragment's matrix ops, so that their latency is covered
+      auto vfrag = [&](int i) -> uint4 {
+        const int vc = (2 * (i >> 1) + ((lr & 3) >> 1)) ^ vsw;  // chunk position of dims 16 dt + 4 (lr % 4)
+        const bf16_t* row = &T.v[((32 * (i & 1) + vr) * NC + vc) * 8 + (lr & 1) * 4];
+        const uint2 lo = ld_tr8(row);
+        const uint2 hi = ld_tr8(row + 16 * D);
+        return make_uint4(lo.x, lo.y, hi.x, hi.y);
+      };
+      uint4 va = vfrag(0);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int vc = (2 * dt + ((lr & 3) >> 1)) ^ vsw;  // chunk position of dims 16 dt + 4 (lr % 4)
+      for (int i = 0; i < 2 * DT; ++i) {
+        const uint4 vn = i + 1 < 2 * DT ? vfrag(i + 1) : va;
 #pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          const bf16_t* row = &T.v[((32 * s + vr) * NC + vc) * 8 + (lr & 1) * 4];
-          const uint2 lo = ld_tr8(row);
-          const uint2 hi = ld_tr8(row + 16 * D);
-          const uint4 va = make_uint4(lo.x, lo.y, hi.x, hi.y);
-#pragma unroll
-          for (int rt = 0; rt < 2; ++rt) acc[rt][dt] = mfma16x16x32(va, pb[rt][s], acc[rt][dt]);
-        }
+        for (int rt = 0; rt < 2; ++rt) acc[rt][i >> 1] = mfma16x16x32(va, pb[rt][i & 1], acc[rt][i >> 1]);
+        va = vn;
       }
     }
   };
