@@ -127,6 +127,18 @@ def _p(a: np.ndarray):
     return a.ctypes.data if a.size else None
 
 
+_SMALL = 64  # int32 arrays up to this length go as ctypes arrays
+
+
+def _i32_small(a):
+    """An int32 array argument as (ctypes array or None, length).  Building a small
+    ctypes array costs well under a microsecond; an ndarray's ``.ctypes.data``
+    costs about two, and a decode call passes two such arrays."""
+    vals = a.tolist() if isinstance(a, np.ndarray) else [int(x) for x in a]
+    n = len(vals)
+    return ((C.c_int32 * n)(*vals) if n else None), n
+
+
 def _dptr(t) -> Optional[int]:
     if t is None:
         return None
@@ -309,21 +321,28 @@ def fcg_patch_prefill(cache: Cache, layer: int, seq, pos, q, k, v, out, stream=N
                                 _dptr(out), _stream(stream) if q is not None else None))
 
 
+def _decode_call(fn, cache: Cache, layer: int, seqs, q, k, v, out, stream) -> np.ndarray:
+    if len(seqs) > _SMALL:
+        s = _i32(seqs)
+        pos = np.zeros(max(s.size, 1), dtype=np.int32)
+        _check(fn(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out), pos.ctypes.data,
+                  _stream(stream) if q is not None else None))
+        return pos[:s.size]
+    # one step of a small batch: the per-call marshalling is a visible part of the step
+    s, n = _i32_small(seqs)
+    pos = (C.c_int32 * max(n, 1))()
+    _check(fn(cache.h, int(layer), n, s, _dptr(q), _dptr(k), _dptr(v), _dptr(out), pos,
+              _stream(stream) if q is not None else None))
+    return np.frombuffer(pos, dtype=np.int32, count=n)
+
+
 def fcg_decode(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.ndarray:
-    s = _i32(seqs)
-    pos = np.zeros(max(s.size, 1), dtype=np.int32)
-    _check(_L.fcg_decode(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v), _dptr(out),
-                         pos.ctypes.data, _stream(stream) if q is not None else None))
-    return pos[:s.size]
+    return _decode_call(_L.fcg_decode, cache, layer, seqs, q, k, v, out, stream)
 
 
 def fcg_decode_noalloc(cache: Cache, layer: int, seqs, q, k, v, out, stream=None) -> np.ndarray:
     """fcg_decode through the entry point that allocates nothing (static device scratch)."""
-    s = _i32(seqs)
-    pos = np.zeros(max(s.size, 1), dtype=np.int32)
-    _check(_L.fcg_decode_noalloc(cache.h, int(layer), int(s.size), _p(s), _dptr(q), _dptr(k), _dptr(v),
-                                 _dptr(out), pos.ctypes.data, _stream(stream) if q is not None else None))
-    return pos[:s.size]
+    return _decode_call(_L.fcg_decode_noalloc, cache, layer, seqs, q, k, v, out, stream)
 
 
 def fcg_cache_timing(cache: Cache, enable: bool) -> None:
