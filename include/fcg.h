@@ -272,8 +272,6 @@ fcg_status fcg_decode_noalloc(fcg_cache* cache, int32_t layer, int32_t n_seqs, c
                               const void* q, const void* k, const void* v, void* out,
                               int32_t* positions_out, void* stream);
 
-/* ------------------------------------------------------------- diagnostics */
-
 /* ------------------------------------------------- code-cache management */
 
 /* Locality score of the cache entries (Sec. 4.1, Eq. 3; App. B.1, Eq. 8-10;
@@ -308,6 +306,8 @@ fcg_status fcg_locality_scores(const fcg_locality* loc, double* scores);
 fcg_status fcg_locality_residency(const fcg_locality* loc, int64_t budget, const int64_t* cost, uint8_t* resident);
 fcg_status fcg_locality_destroy(fcg_locality* loc);
 
+/* ------------------------------------------------------------- diagnostics */
+
 /* Kernel timing (measurement, not part of the method).  While enabled, every
  * call on this cache records HIP events on its stream around its kernels:
  *   FCG_TIME_GRAFT        the graft kernel of fcg_graft
@@ -319,8 +319,8 @@ fcg_status fcg_locality_destroy(fcg_locality* loc);
  * Plan uploads and host work are outside the intervals.  fcg_cache_timing_read
  * waits for the recorded events, returns the number of intervals and their
  * summed duration in milliseconds for one kind (ERANGE for another value),
- * and forgets them.  enable = 0
- * stops recording (recorded intervals stay readable). */
+ * and forgets them.  enable = 0 stops recording (recorded intervals stay
+ * readable). */
 #define FCG_TIME_GRAFT 0
 #define FCG_TIME_PREFILL_ATTN 1
 #define FCG_TIME_PREFILL 2
@@ -329,6 +329,9 @@ fcg_status fcg_locality_destroy(fcg_locality* loc);
 fcg_status fcg_cache_timing(fcg_cache* cache, int32_t enable);
 fcg_status fcg_cache_timing_read(fcg_cache* cache, int32_t kind, int32_t* count, double* total_ms);
 
+/* Name of a status code; the message of the calling thread's last failed
+ * call (kept until its next failure; empty before any).  Both strings are
+ * owned by the library. */
 const char* fcg_status_string(fcg_status s);
 const char* fcg_last_error(void);
 
