@@ -1,13 +1,16 @@
 """Turn rocprofv3 CSV output into the short summaries kept under ``profiles/``.
 
-    python -m paper_2606_13097_amd.profiling stats KERNEL_STATS_CSV --title T --command C
+    python -m paper_2606_13097_amd.profiling stats KERNEL_STATS_CSV --title T --command C \
+        [--trace KERNEL_TRACE_CSV --launches graft_kernel [--launches ...] --note N]
     python -m paper_2606_13097_amd.profiling traffic --kernel graft_kernel --source csrc/k_graft.hip \
         --fetch F.csv --write W.csv --copy-fetch CF.csv --copy-write CW.csv --copy-bytes 1073741824 \
         --skip 1 --command C
     python -m paper_2606_13097_amd.profiling mfma --kernel attn_prefill_mfma_kernel \
         --source csrc/k_attn_mfma.hip --ops OPS.csv --gemm-ops GEMM.csv --gemm-flops 1.37e11 --command C
 
-``traffic`` averages the kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) over its
+``stats`` with ``--trace`` also lists every launch of the named kernels in dispatch order
+(from a kernel trace of the same run, or an excerpt of it with the same columns), so that
+per-phase averages can be read against the bench's own figures.  ``traffic`` averages the kernel's FETCH_SIZE and WRITE_SIZE (KiB per dispatch) over its
 dispatches after the first ``--skip`` ones, and calibrates each counter by what it reads
 for a plain device copy of ``--copy-bytes`` bytes.  ``mfma`` does the same for the bf16
 matrix-op counter SQ_INSTS_VALU_MFMA_MOPS_BF16, calibrated by a bf16 GEMM of known FLOPs
@@ -56,6 +59,22 @@ def stats_markdown(path: str, title: str, command: str) -> str:
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
                      f"{float(r['TotalDurationNs']) / 1e6:.2f} |")
     return "\n".join(lines) + "\n"
+
+
+def launches_markdown(trace: str, kernels, note: str = "") -> str:
+    """Every launch of each named kernel, in dispatch order: duration in microseconds."""
+    rows = list(csv.DictReader(open(trace)))
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    out = []
+    for k in kernels:
+        d = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows if k in r["Kernel_Name"]]
+        if not d:
+            continue
+        out += ["", f"{k}: {len(d)} launches in dispatch order (us):", "",
+                "    " + ", ".join(f"{x:.1f}" for x in d)]
+    if out and note:
+        out += ["", note]
+    return "\n".join(out) + ("\n" if out else "")
 
 
 def _per_dispatch(path: str, kernel: str, counter: str):
@@ -113,6 +132,9 @@ def main(argv=None):
     s.add_argument("csv")
     s.add_argument("--title", required=True)
     s.add_argument("--command", required=True)
+    s.add_argument("--trace", default=None, help="kernel trace CSV of the same run")
+    s.add_argument("--launches", action="append", default=[], help="kernel whose launches to list")
+    s.add_argument("--note", default="")
     t = sub.add_parser("traffic")
     for k in ("kernel", "source", "fetch", "write", "copy_fetch", "copy_write", "command"):
         t.add_argument("--" + k.replace("_", "-"), dest=k, required=True)
@@ -129,6 +151,8 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         sys.stdout.write(stats_markdown(a.csv, a.title, a.command))
+        if a.trace and a.launches:
+            sys.stdout.write(launches_markdown(a.trace, a.launches, a.note))
     else:
         json.dump(traffic(a) if a.cmd == "traffic" else mfma(a), sys.stdout, indent=1)
         sys.stdout.write("\n")
