@@ -380,7 +380,7 @@ def cpu_baseline(task_ws, seed):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: this build runs the grafting path on a single MI355X "
+        print(f"bench.py measures one GPU only: the grafting path runs on a single MI355X "
               f"with no sharding (asked for --gpus {args.gpus})", file=sys.stderr)
         sys.exit(2)
     import numpy as np

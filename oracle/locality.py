@@ -21,8 +21,8 @@ Readings where the paper leaves a choice:
     invocation of f within one trace (so sum_j l_asso(j | f) is the share of
     f's invocations that another call follows, within [0, 1]);
   - l_curr(f) = 1 iff f occurs in the most recent trace;
-  - a component whose denominator is 0 is 0; PPL values are supplied (the
-    model that would measure them is not part of this build);
+  - a component whose denominator is 0 is 0; PPL values are supplied by the
+    caller (the language model that would measure them is out of scope);
   - residency (Alg. 1, the update step): functions in descending score, ties
     by ascending id, are kept on the GPU while their summed cost fits the
     budget; a function that does not fit is skipped and later ones are still
