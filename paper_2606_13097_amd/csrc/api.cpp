@@ -985,9 +985,15 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
   // pair mode with splits under 8 tiles: the call is bound by latency, not by
   // the matrix work, and planning for one block per CU halves the splits the
   // combine merges (7B patch: call 35 -> 31 us, the attention kernel unchanged).
-  // The blocks keep the two-tile ring: the deeper rings need more registers
-  // than 4-wave blocks have without AGPR copies, and were 10-15% slower.
-  if (pair && per < 8) per = split_tiles(256);
+  // The 128-row blocks run as 8 waves of 16 rows (two waves per SIMD, each
+  // with one row tile; 4 waves of 32 rows left one wave per SIMD: attention
+  // kernel 16.0 -> 15.0 us) and keep the two-tile ring (the four-tile ring
+  // measured no faster).
+  bool pair_one = false;
+  if (pair && per < 8) {
+    per = split_tiles(256);
+    pair_one = true;
+  }
   const int nbuf = pair ? 2 : 4;
   const int64_t span = per * tile;
   std::vector<AttnItem> items;                 // VALU path: one item per (row block, split)
@@ -1076,7 +1082,7 @@ fcg_status run_attention(fcg_cache* c, int32_t layer, const std::vector<TokenMet
     for (size_t li = 0; li < pf_launch.size(); ++li) {
       const KTime tm{li == 0 ? e_attn0 : nullptr, li + 1 == pf_launch.size() ? e_attn1 : nullptr};
       rc = launch_attn_mfma(pf_launch[li], dmeta, c->qws, n * g, cv, layer, d.n_q_heads, out, part_o, part_ml,
-                            stride_rows, nbuf, s, tm, fin);
+                            stride_rows, nbuf, s, tm, fin, pair_one ? 16 : 32);
       if (rc) break;
     }
   } else

@@ -97,14 +97,17 @@ __device__ __forceinline__ uint2 ld_tr8(const bf16_t* p) {
   return __builtin_bit_cast(uint2, x);
 }
 
-// grid (row block, key split, kv head).  NBUF tiles in the LDS ring: 4 (three
-// in flight while one is attended) for 8-wave blocks and 4-wave blocks of the
-// plain one-per-CU plan, 2 (132 KB against 68 KB of LDS at D 128) for 4-wave
-// blocks planned two per CU, whose phases then overlap (one block's softmax
-// beside the other's matrix work).  4-wave blocks aim at 256 registers per
-// lane (two waves per SIMD); the four-tile ring at D 128 still needs more,
+// grid (row block, key split, kv head).  Each wave attends RT 16-row tiles
+// of the block's query rows (WAVES * RT * 16 rows).  NBUF tiles in the LDS
+// ring: 4 (three in flight while one is attended) for 8-wave blocks of 32-row
+// waves and 4-wave blocks of the plain one-per-CU plan, 2 (132 KB against
+// 68 KB of LDS at D 128) for 4-wave blocks planned two per CU, whose phases
+// then overlap (one block's softmax beside the other's matrix work), and for
+// 128-row blocks of 8 waves x 16 rows planned one per CU (two waves per SIMD
+// again, each with half the row tiles).  4-wave blocks aim at 256 registers
+// per lane (two waves per SIMD); the four-tile ring at D 128 still needs more,
 // and the compiler keeps its accumulators in AGPRs.
-template <int D, bool PAGED, int WAVES, int NBUF, bool FUSED>
+template <int D, bool PAGED, int WAVES, int NBUF, bool FUSED, int RT>
 __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_mfma_kernel(
     PrefillArgs args, const TokenMeta* __restrict__ meta, const bf16_t* __restrict__ qws, int rows_ws,
     CacheView cv, int layer, int Hq, bf16_t* __restrict__ out, float* __restrict__ part_o,
@@ -277,15 +280,15 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   issue_to(0, tiles[0]);  // ntiles >= 1: the split is not empty
   // query rows of this lane: one per 16-row tile (rows past the block's last
   // one load row 0 and are never written)
-  int rpos[2], rtok[2];  // position (of row 0 for rows past the block) and token of the lane's rows
-  uint4 qf[2][KS];
+  int rpos[RT], rtok[RT];  // position (of row 0 for rows past the block) and token of the lane's rows
+  uint4 qf[RT][KS];
   // fused: the raw query dims of the lane, encoded once they and tile 0 have
   // landed.  The rotary partner of dims d (d +- D/2) is the lane's own k step
   // ks ^ (D / 64).
-  uint4 qa[2][FUSED ? KS : 1];
+  uint4 qa[RT][FUSED ? KS : 1];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
-    const int r = 32 * w + 16 * rt + lr;
+  for (int rt = 0; rt < RT; ++rt) {
+    const int r = 16 * (RT * w + rt) + lr;
     const int rl = r < rows ? r : 0;
     if constexpr (FUSED) {
       // the block's tokens are consecutive positions from rmin, consecutive caller indices
@@ -314,7 +317,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     }
     const uint4* cs_lds = reinterpret_cast<const uint4*>(&tiles[kNBuf - 1]);
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+    for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int d = ks * 32 + lq * 8;
@@ -341,7 +344,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       }
   }
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) asm volatile("" ::"v"(__builtin_bit_cast(u32x4_t, qf[rt][ks])));
     asm volatile("" ::"v"(rpos[rt]), "v"(rtok[rt]));
@@ -349,11 +352,15 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 #pragma unroll
   for (int i = 1; i < kNBuf - 1; ++i)
     if (i < ntiles) issue_to(i, tiles[i]);
-  float mrow[2] = {-INFINITY, -INFINITY};
-  float lsum[2] = {0.f, 0.f};
-  floatx4 acc[2][DT];
+  float mrow[RT], lsum[RT];
+  floatx4 acc[RT][DT];
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt)
+  for (int rt = 0; rt < RT; ++rt) {
+    mrow[rt] = -INFINITY;
+    lsum[rt] = 0.f;
+  }
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
@@ -435,7 +442,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     {
       const int kb = k0 + tile * kBN;
       // S^T = K Q^T: four 16-key tiles x two 16-row tiles
-      floatx4 st[2][4];
+      floatx4 st[RT][4];
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         uint4 ka[KS];
@@ -445,7 +452,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
           ka[ks] = ld16(&T.k[(r * NC + ((ks * 4 + lq) ^ Tile::swz_k(r))) * 8]);
         }
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < RT; ++rt) {
           floatx4 c = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int ks = 0; ks < KS; ++ks) c = mfma16x16x32(ka[ks], qf[rt][ks], c);
@@ -456,13 +463,13 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       // first query position or the split's end (a block-uniform branch)
       if (kb + kBN > kend || kb + kBN - 1 > rb.rmin) {
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
+        for (int rt = 0; rt < RT; ++rt) {
           // key kb + 16 kt + 4 lq + e is visible iff 16 kt + e <= lim.  The
           // empty asm keeps the compiler from hoisting this out of the loop,
           // which would wait for the metadata load before the first K/V load.
           int rp = rpos[rt];
           asm volatile("" : "+v"(rp));
-          rp = 32 * w + 16 * rt + lr < rows ? rp : -1;
+          rp = 16 * (RT * w + rt) + lr < rows ? rp : -1;
           const int lim = min(rp, kend - 1) - kb - 4 * lq;
 #pragma unroll
           for (int kt = 0; kt < 4; ++kt)
@@ -470,9 +477,9 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
             for (int e = 0; e < 4; ++e) st[rt][kt][e] = (16 * kt + e <= lim) ? st[rt][kt][e] : -INFINITY;
         }
       }
-      uint4 pb[2][2];
+      uint4 pb[RT][2];
 #pragma unroll
-      for (int rt = 0; rt < 2; ++rt) {
+      for (int rt = 0; rt < RT; ++rt) {
         float tmax = -INFINITY;
 #pragma unroll
         for (int kt = 0; kt < 4; ++kt)
@@ -532,7 +539,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       for (int i = 0; i < 2 * DT; ++i) {
         const uint4 vn = i + 1 < 2 * DT ? vfrag(i + 1) : va;
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) acc[rt][i >> 1] = mfma16x16x32(va, pb[rt][i & 1], acc[rt][i >> 1]);
+        for (int rt = 0; rt < RT; ++rt) acc[rt][i >> 1] = mfma16x16x32(va, pb[rt][i & 1], acc[rt][i >> 1]);
         va = vn;
       }
     }
@@ -560,9 +567,9 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 
   // epilogue: lane holds O^T[d = 16 dt + 4 lq + e][row lr] of each row tile
 #pragma unroll
-  for (int rt = 0; rt < 2; ++rt) {
+  for (int rt = 0; rt < RT; ++rt) {
     const float l = sum_rows4(lsum[rt]);
-    const int r = 32 * w + 16 * rt + lr;
+    const int r = 16 * (RT * w + rt) + lr;
     if (r >= rows) continue;
     if (part < 0) {
       const float inv = l > 0.f ? 1.f / l : 0.f;
@@ -580,7 +587,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       // stores, read once by the merge kernel
       const int64_t pr = ((int64_t)part * Hkv + hk) * part_stride_rows + r;
       bf16_t* o = reinterpret_cast<bf16_t*>(part_o) + ((int64_t)part * Hkv + hk) * part_stride_rows * D +
-                  ((int64_t)(2 * w + rt) * DT * 64 + lane) * 4;
+                  ((int64_t)(RT * w + rt) * DT * 64 + lane) * 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const floatx4 a = acc[rt][dt];
@@ -596,20 +603,32 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm, FusedIn fin) {
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm, FusedIn fin, int wave_rows) {
   if (args.n_rb == 0 || args.n_split == 0) return 0;
   const int groups = args.n_split * cv.n_kv_heads;  // (split, kv head) pairs
   const dim3 grid = args.xcd_group ? dim3(kXcds * args.n_rb, (groups + kXcds - 1) / kXcds)
                                    : dim3(args.n_rb, args.n_split, cv.n_kv_heads);
-  const int waves = part_stride_rows / 32;      // rows per block / 32
-  if ((nbuf != 2 && nbuf != 4) || (nbuf == 2 && waves != 4)) return (int)hipErrorInvalidValue;
+  if (wave_rows != 16 && wave_rows != 32) return (int)hipErrorInvalidValue;
+  const int waves = part_stride_rows / wave_rows;  // rows per block / rows per wave
+  // instances: 128-row blocks of 4 waves (two-tile ring: two per CU; four-tile
+  // ring: one per CU), 128-row blocks of 8 waves x 16 rows (two-tile ring, one
+  // per CU), 256-row blocks of 8 waves (four-tile ring)
+  const bool ok = wave_rows == 32 ? (waves == 4 && (nbuf == 2 || nbuf == 4)) || (waves == 8 && nbuf == 4)
+                                  : waves == 8 && nbuf == 2;
+  if (!ok) return (int)hipErrorInvalidValue;
   const bool fused = fin.q != nullptr;
-#define PF(DD, PG, WV, NB, FU)                                                                                \
-  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB, FU>), grid, dim3(WV * 64), 0, s, tm.start,   \
-                        tm.stop, 0, args, meta, (const bf16_t*)qws, rows_ws, cv, layer, Hq, (bf16_t*)out,       \
-                        part_o, part_ml, part_stride_rows, (const bf16_t*)fin.q, (const bf16_t*)fin.k,          \
-                        (const bf16_t*)fin.v, fin.rope)
-#define PFS(DD, PG, FU) { if (nbuf == 2) PF(DD, PG, 4, 2, FU); else if (waves == 8) PF(DD, PG, 8, 4, FU); else PF(DD, PG, 4, 4, FU); }
+#define PF(DD, PG, WV, NB, FU, RR)                                                                            \
+  hipExtLaunchKernelGGL((attn_prefill_mfma_kernel<DD, PG, WV, NB, FU, RR>), grid, dim3(WV * 64), 0, s,         \
+                        tm.start, tm.stop, 0, args, meta, (const bf16_t*)qws, rows_ws, cv, layer, Hq,           \
+                        (bf16_t*)out, part_o, part_ml, part_stride_rows, (const bf16_t*)fin.q,                  \
+                        (const bf16_t*)fin.k, (const bf16_t*)fin.v, fin.rope)
+#define PFS(DD, PG, FU)                                                                                       \
+  {                                                                                                           \
+    if (wave_rows == 16) PF(DD, PG, 8, 2, FU, 1);                                                             \
+    else if (nbuf == 2) PF(DD, PG, 4, 2, FU, 2);                                                              \
+    else if (waves == 8) PF(DD, PG, 8, 4, FU, 2);                                                             \
+    else PF(DD, PG, 4, 4, FU, 2);                                                                             \
+  }
 #define PFW(DD, PG) { if (fused) PFS(DD, PG, true) else PFS(DD, PG, false) }
   const bool paged = cv.page_size != 0;
   if (cv.head_dim == 128) { if (paged) PFW(128, true) else PFW(128, false) }

@@ -178,8 +178,9 @@ struct PrefillArgs {
 };
 
 // bf16 MFMA attention of query-workspace rows over the cache.  Blocks of
-// part_stride_rows / 32 waves; nbuf: tiles of the LDS ring, 2 for 4-wave
-// blocks sized to run two per CU, else 4.
+// part_stride_rows / wave_rows waves (wave_rows 32, or 16: 128-row blocks of 8
+// waves, two per SIMD, for blocks planned one per CU); nbuf: tiles of the LDS
+// ring, 2 for 128-row blocks planned two per CU or of 16-row waves, else 4.
 // Fused launches take the caller's fresh q [n][Hq][D], k, v [n][Hkv][D] and the
 // cache's rotary table instead of the query workspace: queries are encoded in
 // the kernel's prologue, fresh keys and values are read from the inputs (keys
@@ -193,7 +194,8 @@ struct FusedIn {
 };
 int launch_attn_mfma(const PrefillArgs& args, const TokenMeta* meta, const void* qws, int rows_ws,
                      const CacheView& cv, int layer, int Hq, void* out, float* part_o, float* part_ml,
-                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm = {}, FusedIn fin = {});
+                     int part_stride_rows, int nbuf, hipStream_t s, KTime tm = {}, FusedIn fin = {},
+                     int wave_rows = 32);
 
 // VALU attention, one token (g query rows) per item; any dtype.
 int launch_attn_rows(int dtype, const AttnItem* items, int n_items, const TokenMeta* meta, const void* qws,
