@@ -1131,10 +1131,15 @@ DecodePlan plan_decode(const fcg_model_desc& d, int32_t n, const std::vector<int
   // 256 keys per block (fewer partials for the merge in each (sequence, kv
   // head)'s last block), two per compute unit for more keys (shorter key
   // loops) -- rounded up to whole 64-key chunks; at most 256 splits per
-  // sequence
-  const int64_t target_blocks = total * d.n_kv_heads <= 256 * 256 ? 256 : 512;
+  // sequence, and at most 32 when planning two blocks per compute unit: past
+  // that the last block's fold of the partials costs more than the shorter
+  // key loops save (16.7K-token context at batch 1: 53 splits 20.4 us per
+  // call, 30 splits 19.1 us)
+  const bool two_per_cu = total * d.n_kv_heads > 256 * 256;
+  const int64_t target_blocks = two_per_cu ? 512 : 256;
+  const int64_t max_splits = two_per_cu ? 32 : 256;
   int64_t sk = std::max<int64_t>(64, (total * d.n_kv_heads + target_blocks - 1) / target_blocks);
-  sk = std::max<int64_t>(sk, (pmax + 1 + 255) / 256);
+  sk = std::max<int64_t>(sk, (pmax + 1 + max_splits - 1) / max_splits);
   for (;;) {
     int64_t blocks = 0;
     for (int32_t i = 0; i < n; ++i) blocks += (pos[i] + sk) / sk;
