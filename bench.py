@@ -69,8 +69,11 @@ def measured_counter(name, field):
     return int(round(d[field]))
 
 
-def measured_traffic(name):
-    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated by a plain copy)."""
+def measured_traffic(name, workload=None):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, calibrated by a plain copy), from the summary
+    taken on ``workload``; None for another workload (the counters are per workload)."""
+    if workload is not None and f"_{workload}_" not in name:
+        return None
     return measured_counter(name, "traffic_bytes_per_launch")
 
 
@@ -617,7 +620,7 @@ def main():
                   "the timed pass and include host work and plan uploads",
         "roofline": {"bound": "hbm", "kernel": "fcg graft_kernel", "achieved": round(graft_gbs, 2),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(graft_gbs / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("graft_7b_traffic.json"),
+                     "traffic": None if args.alias_v else measured_traffic(f"graft_{args.workload}_traffic.json", args.workload),
                      "algorithmic_bytes_per_launch": int(round(g_bytes / K))},
         "roofline_patch_attn": (
             {"bound": "hbm", "kernel": "fcg attn_prefill_mfma_kernel", "achieved": round(attn_gbs, 2),
@@ -625,8 +628,9 @@ def main():
             if p_bound == "hbm" else
             {"bound": "mfma", "kernel": "fcg attn_prefill_mfma_kernel", "achieved": round(attn_tflops, 3),
              "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / BF16_PEAK_TFLOPS, 4)}) | {
-            "traffic": measured_traffic("prefill_7b_traffic.json"),
-            "counter_flops_per_launch": measured_counter("prefill_7b_mfma.json", "counter_flops_per_launch"),
+            "traffic": measured_traffic("prefill_7b_traffic.json", args.workload),
+            "counter_flops_per_launch": (measured_counter("prefill_7b_mfma.json", "counter_flops_per_launch")
+                                         if args.workload == "7b" else None),
             "algorithmic_flops_per_launch": int(round(p_flops / (K * sh.n_layers))),
             "algorithmic_bytes_per_launch": int(round(p_bytes / (K * sh.n_layers))),
             "intensity_flop_per_byte": round(p_intensity, 1),
@@ -634,7 +638,7 @@ def main():
             "hbm_frac": round(attn_gbs / HBM_PEAK_GBS, 4)},
         "roofline_decode": {"bound": "hbm", "kernel": "fcg decode_mfma_kernel" if sh.dtype == "bf16" else "fcg decode_kernel", "achieved": round(decode_attn_gbs, 2),
                             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(decode_attn_gbs / HBM_PEAK_GBS, 4),
-                            "traffic": measured_traffic("decode_7b_traffic.json"),
+                            "traffic": measured_traffic("decode_7b_traffic.json", args.workload),
                             "algorithmic_bytes_per_launch": int(round(d_bytes / n_dec_calls))},
     }
     res["locality"] = locality_update(w, task_ws)
