@@ -2,17 +2,19 @@
 // span attends over the reused prefix KV states).  bf16 operands, fp32
 // accumulation, fp32 online softmax in base 2.
 //
-// Block: 4 or 8 waves, 32 query rows each, of one kv head (the g query heads
-// of consecutive tokens of one sequence), and one split [k0, k1) of the key
-// positions.  Wave w owns rows 32w .. 32w + 31 as two 16-row tiles.  The host
-// picks the shape per call: 4-wave blocks sized to run two per CU (the two
-// blocks' softmax and matrix phases overlap), or, when 256-row blocks alone
-// fill the chip twice, 8-wave blocks one per CU.
+// Block: 4 or 8 waves of one kv head (the g query heads of consecutive tokens
+// of one sequence) and one split [k0, k1) of the key positions.  Wave w owns
+// RT 16-row tiles of query rows, rows 16 RT w .. 16 RT (w + 1) - 1.  The host
+// picks the shape per call: 128-row blocks of 4 waves x 32 rows sized to run
+// two per CU (the two blocks' softmax and matrix phases overlap); the same
+// rows as 8 waves x 16 rows, one block per CU, when short key splits make the
+// call latency-bound; or, when 256-row blocks alone fill the chip twice, 8
+// waves x 32 rows one per CU.
 //
 // Key tiles of 64 keys go from memory straight into LDS (global_load_lds:
-// each instruction fills 1 KB, 16 bytes per lane), into a ring of four
-// single-tile buffers, so three tiles are in flight while one is attended and
-// staging costs no registers.  K and V keep their [key][D] rows; the 16-byte
+// each instruction fills 1 KB, 16 bytes per lane), into a ring of two or four
+// single-tile buffers, so up to three tiles are in flight while one is
+// attended and staging costs no registers.  K and V keep their [key][D] rows; the 16-byte
 // chunks of each row are XOR-swizzled so that the reads below meet no bank
 // conflicts.  Then per tile:
 //   - S^T = K Q^T with v_mfma_f32_16x16x32_bf16 (A = K from LDS, B = Q^T held
