@@ -63,3 +63,24 @@ def test_source_hash_covers_every_listed_file():
     a = profiling.source_sha256("csrc/k_decode_mfma.hip")
     ab = profiling.source_sha256("csrc/k_decode_mfma.hip+csrc/decode_common.hpp")
     assert a != ab and len(ab) == 64
+
+
+def test_bench_reports_counter_traffic_only_for_the_workload_it_was_taken_on():
+    """The committed traffic summaries are per workload: a bench line of another workload
+    carries no traffic figure rather than the 7B one."""
+    import importlib.util
+    import os
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    spec = importlib.util.spec_from_file_location("fcg_bench", os.path.join(root, "bench.py"))
+    bench = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(bench)
+    assert bench.measured_traffic("graft_long16k_traffic.json", "long16k") is None   # no such summary
+    assert bench.measured_traffic("prefill_7b_traffic.json", "34b") is None
+    assert bench.measured_traffic("graft_batched_traffic.json", "7b") is None
+    got = bench.measured_traffic("prefill_7b_traffic.json", "7b")
+    with open(os.path.join(root, "profiles", "prefill_7b_traffic.json")) as f:
+        d = json.load(f)
+    if d["source_sha256"] == profiling.source_sha256(d["source"]):
+        assert got == int(round(d["traffic_bytes_per_launch"]))
+    else:                                   # kernel changed since the counters were taken
+        assert got is None
