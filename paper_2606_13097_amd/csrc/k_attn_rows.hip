@@ -166,8 +166,9 @@ __global__ void __launch_bounds__(256) attn_rows_kernel(const AttnItem* __restri
 // taking interleaved splits, their sums added through LDS).
 constexpr int kCombRows = 8;
 constexpr int kCombMaxParts = 256;
-// PRE: 16 when no row block of the launch has more splits (each preload past
-// the last split re-reads it: 7B patch call -0.4 us against 32), else 32.
+// PRE: the smallest of 4, 16 and 32 that covers every row block of the
+// launch (each preload past the last split re-reads it: 7B patch call -0.4 us
+// with 16 against 32).
 template <typename T, int D, bool MFMA_PART, int PRE>
 __global__ void __launch_bounds__(256) combine_kernel(CombineArgs args, const TokenMeta* __restrict__ meta, int Hq,
                                                       int Hkv, const float* __restrict__ part_o,
@@ -321,14 +322,15 @@ int launch_combine(int dtype, const CombineArgs& args, const TokenMeta* meta, in
   dim3 grid(args.n_items, Hkv, (part_stride_rows + kCombRows - 1) / kCombRows);
   int max_np = 0;
   for (int i = 0; i < args.n_items; ++i) max_np = max(max_np, (int)args.item[i].n_part);
-  const bool pre16 = max_np <= 16;
+  const int pre = max_np <= 4 ? 4 : max_np <= 16 ? 16 : 32;
 #define CBK(T, DD, MP, PR)                                                                                  \
   hipExtLaunchKernelGGL((combine_kernel<T, DD, MP, PR>), grid, dim3(256), 0, s, tm.start, tm.stop, 0, args,   \
                         meta, Hq, Hkv, part_o, part_ml, part_stride_rows, (T*)out)
 #define CB(T, DD)                                                                                            \
   do {                                                                                                       \
     if (!mfma_part) CBK(T, DD, false, 16);                                                                   \
-    else if (pre16) CBK(T, DD, true, 16);                                                                    \
+    else if (pre == 4) CBK(T, DD, true, 4);                                                                  \
+    else if (pre == 16) CBK(T, DD, true, 16);                                                                \
     else CBK(T, DD, true, 32);                                                                               \
   } while (0)
   if (dtype == 0) { if (D == 64) CB(float, 64); else CB(float, 128); }
