@@ -211,14 +211,14 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   const bf16_t* kbase = ck + head_base;
   const bf16_t* vbase = cvv + head_base;
   // rows of positions in [k0, kend)
-  auto krow = [&](int p) -> const bf16_t* {
+  auto krow = [&](int p) -> const bf16_t* __attribute__((always_inline)) {
     if (!PAGED) return kbase + p * D;
     if (window)
       return ck + (int64_t)layer * cv.layer_stride +
              (((int64_t)s_pg[(p >> 4) - lpa] * Hkv + hk) * 16 + (p & 15)) * D;
     return ck + kv_offset<true>(cv, layer, rb.seq, hk, p);
   };
-  auto vrow = [&](int p) -> const bf16_t* {
+  auto vrow = [&](int p) -> const bf16_t* __attribute__((always_inline)) {
     if (!PAGED) return vbase + p * D;
     if (window) {
       const int e = (p >> 4) - lpa;
@@ -231,7 +231,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
     return v_row<true, bf16_t>(cv, layer, rb.seq, hk, p);
   };
   // the cache's own value row of position p (fresh tokens' pages are never read from the library)
-  auto vown = [&](int p) -> const bf16_t* {
+  auto vown = [&](int p) -> const bf16_t* __attribute__((always_inline)) {
     if (!PAGED) return vbase + p * D;
     if (window)
       return cvv + (int64_t)layer * cv.layer_stride + (((int64_t)s_pg[(p >> 4) - lpa] * Hkv + hk) * 16 + (p & 15)) * D;
@@ -243,7 +243,7 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
   // position (64 j' + l) % NC, so it loads the chunk that the swizzle puts
   // there.  Keys past the split read its last key (valid memory; masked).
   const int ntiles = (kend - k0 + kBN - 1) / kBN;
-  auto issue_to = [&](int tile, Tile& B) {
+  auto issue_to = [&](int tile, Tile& B) __attribute__((always_inline)) {
     const int kb = k0 + tile * kBN;
 #pragma unroll
     for (int u = 0; u < DPT; ++u) {
@@ -366,10 +366,10 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) acc[rt][dt] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  // One tile, in ring buffer `buf`: a std::integral_constant on the unrolled
-  // path (each step its own instantiation, every LDS address a constant
-  // offset from a per-lane base), a plain int on the paged path.
-  auto step = [&](int tile, auto buf) {
+  // One tile, in ring buffer `buf`, a std::integral_constant (each step of the
+  // unrolled loop its own instantiation, every LDS address a constant offset
+  // from a per-lane base).
+  auto step = [&](int tile, auto buf) __attribute__((always_inline)) {
     const Tile& T = tiles[buf];
     // this wave's loads of the tile have landed (the later tiles in flight,
     // up to kNBuf - 2 of them, may still be pending) ...
@@ -546,25 +546,21 @@ __global__ void __launch_bounds__(WAVES * 64, WAVES == 4 ? 2 : 1) attn_prefill_m
       }
     }
   };
-  if constexpr (!PAGED) {
-    // contiguous caches: the loop is unrolled by the ring size, so each step's
-    // buffers are fixed and every LDS address is a constant offset from a
-    // per-lane base (long-context and 34B-shape prefill +4-7%)
-    for (int t0 = 0; t0 < ntiles; t0 += kNBuf) {
-      step(t0, std::integral_constant<int, 0>{});
-      if (t0 + 1 >= ntiles) break;
-      step(t0 + 1, std::integral_constant<int, 1>{});
-      if constexpr (kNBuf == 4) {
-        if (t0 + 2 >= ntiles) break;
-        step(t0 + 2, std::integral_constant<int, 2 % kNBuf>{});
-        if (t0 + 3 >= ntiles) break;
-        step(t0 + 3, std::integral_constant<int, 3 % kNBuf>{});
-      }
+  // The loop is unrolled by the ring size, so each step's buffers are fixed and
+  // every LDS address is a constant offset from a per-lane base (long-context
+  // and 34B-shape prefill +4-7%).  The lambdas are forced inline: outlined, as
+  // the compiler once chose for the paged instances, they kept a stack object
+  // in scratch and those instances ran 6x slower.
+  for (int t0 = 0; t0 < ntiles; t0 += kNBuf) {
+    step(t0, std::integral_constant<int, 0>{});
+    if (t0 + 1 >= ntiles) break;
+    step(t0 + 1, std::integral_constant<int, 1>{});
+    if constexpr (kNBuf == 4) {
+      if (t0 + 2 >= ntiles) break;
+      step(t0 + 2, std::integral_constant<int, 2 % kNBuf>{});
+      if (t0 + 3 >= ntiles) break;
+      step(t0 + 3, std::integral_constant<int, 3 % kNBuf>{});
     }
-  } else {
-    // paged caches: unrolled, the paged instances kept a stack object (384 bytes
-    // of scratch per lane) and ran 6x slower
-    for (int tile = 0; tile < ntiles; ++tile) step(tile, tile % kNBuf);
   }
 
   // epilogue: lane holds O^T[d = 16 dt + 4 lq + e][row lr] of each row tile
